@@ -1,0 +1,239 @@
+#!/usr/bin/env python3
+"""Benchmark of the MoE decode expert stage on one MI355X.
+
+One step = one decode token through every MoE layer of the workload: router gating,
+cache check + LRU update, SwiGLU FFN of cache-hit experts on the GPU, missed experts
+on the host thread pool, post-fetch of missed experts into the cache, weighted
+combine (Section III-A steps 1-3). Inputs (router weights, expert weights, AR(1)
+hidden states) are synthetic and seeded; expert weights live in pinned host memory
+(the full model) and in the per-layer GPU expert cache (M of n experts per layer),
+starting cold. The warmup steps fill the cache; the timed steps run the real LRU
+trace, so they include host-side misses and post-fetch copies.
+
+Prints one JSON line. `value` is MoE-stage tokens/s (all layers; attention is not
+part of the stage). `roofline` is the gate/up/SiLU kernel (the largest share of the
+weight stream) timed with HIP events on the compute stream over the timed steps,
+against the MI355X HBM peak. `cpu_baseline` times the oracle (plain CPU reference)
+on a bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def build_world(torch, moe, synth, wl, steps_total, seed, threads):
+    import numpy as np
+    d, f, n, k, L, M = wl.d, wl.f, wl.n, wl.k, wl.L, wl.ways
+    stride = moe.slab_bytes(d, f)
+    t0 = time.perf_counter()
+    host = moe.PinnedBuffer(L * n * stride)
+    log(f"pinned host experts: {L * n * stride / 1e9:.1f} GB in {time.perf_counter() - t0:.1f}s")
+    hview = torch.from_numpy(host.array)
+    tmp = torch.empty(3 * d * f, dtype=torch.bfloat16, device="cuda")
+    for l in range(L):
+        for e in range(n):
+            synth.expert_slab_torch(synth.seed_for(seed, wl.name, "expert", l, e), d, f, wl.w_std, out=tmp)
+            off = (l * n + e) * stride
+            hview[off: off + 3 * d * f * 2].copy_(tmp.view(torch.uint8))
+    del tmp
+    log(f"expert weights drawn: {time.perf_counter() - t0:.1f}s")
+    shared = None
+    if wl.f_shared:
+        sstride = moe.slab_bytes(d, wl.f_shared)
+        shared = torch.zeros(L * sstride, dtype=torch.uint8, device="cuda")
+        for l in range(L):
+            t = shared[l * sstride: l * sstride + 3 * d * wl.f_shared * 2].view(torch.bfloat16)
+            synth.expert_slab_torch(synth.seed_for(seed, wl.name, "shared", l, 0), d, wl.f_shared, wl.w_std, out=t)
+    wr = torch.stack([synth.router_weights_torch(synth.seed_for(seed, wl.name, "router", l), n, d)
+                      for l in range(L)]).contiguous()
+    X = np.stack([synth.ar1_states(synth.seed_for(seed, wl.name, "states", l), steps_total, d) for l in range(L)])
+    xd = torch.from_numpy(np.ascontiguousarray(X.transpose(1, 0, 2))).cuda()     # [T, L, d]
+    pool = torch.zeros(L * M * stride, dtype=torch.uint8, device="cuda")
+    cache = moe.Cache(L, n, M, k)
+    hp = moe.HostPool(threads)
+    rt = moe.Runtime(d, f, n, k, M, L, wr, pool, [host.ptr + i * stride for i in range(L * n)], cache, hp,
+                     f_shared=wl.f_shared, shared_pool=shared)
+    torch.cuda.synchronize()
+    log(f"world ready in {time.perf_counter() - t0:.1f}s (device cache {pool.numel() / 1e9:.1f} GB)")
+    return dict(host=host, wr=wr, X=X, xd=xd, pool=pool, shared=shared, cache=cache, hp=hp, rt=rt, stride=stride)
+
+
+def cpu_baseline(wl, world, seed, budget_s, t_first):
+    """The oracle (plain CPU reference) on a bounded sample of the same workload:
+    consecutive tokens of layers 0, 1, ... (router, chosen experts, combine, LRU),
+    until about budget_s seconds of CPU work; scaled to tokens/s over all layers."""
+    import numpy as np
+    import oracle
+    from oracle import lru as olru
+    wr = world["wr"].cpu().numpy()
+    X = world["X"]
+    host, stride = world["host"], world["stride"]
+    d, f, n, k, L = wl.d, wl.f, wl.n, wl.k, wl.L
+    shared_np = None
+    if wl.f_shared:
+        sstride = moe_slab_bytes(d, wl.f_shared)
+        shared_np = world["shared"].cpu().numpy()
+    threads = oracle.get_threads()
+    done, elapsed = 0, 0.0
+    layers_used = set()
+    T = X.shape[1]
+    order = [(l, t) for l in range(L) for t in range(t_first, T)]
+    cache = olru.LRUCache(L, wl.ways)
+    for (l, t) in order:
+        slabs = [host.array[(l * n + e) * stride:(l * n + e) * stride + 3 * d * f * 2].view(np.uint16)
+                 for e in range(n)]
+        sh = None
+        if shared_np is not None:
+            sh = shared_np[l * sstride: l * sstride + 3 * d * wl.f_shared * 2].view(np.uint16)
+        t0 = time.perf_counter()
+        idx, w, out, gap = oracle.moe_token(X[l, t], wr[l], slabs, k, f, shared_slab=sh, f_shared=wl.f_shared)
+        cache.access(l, list(idx))
+        elapsed += time.perf_counter() - t0
+        done += 1
+        layers_used.add(l)
+        if elapsed >= budget_s:
+            break
+    per_token_layer = elapsed / done
+    return {
+        "value": 1.0 / (per_token_layer * L), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+        "sample": (f"{done} token-layers (layers {min(layers_used)}-{max(layers_used)}, consecutive tokens from "
+                   f"step {t_first}) through router + top-{k} SwiGLU experts + combine + LRU, "
+                   f"{elapsed:.1f}s; scaled to {L} layers per token"),
+        "ms_per_token_layer": per_token_layer * 1e3,
+    }
+
+
+def moe_slab_bytes(d, f):
+    import paper_2512_16473_amd as moe
+    return moe.slab_bytes(d, f)
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=32)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--workload", default="mixtral", choices=["mixtral", "phi", "fine", "tiny"])
+    ap.add_argument("--threads", type=int, default=0, help="host expert threads (0: OMP_NUM_THREADS or all cores)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-baseline-s", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: the decode expert stage has no multi-GPU path here "
+              f"(--gpus {args.gpus} requested).", file=sys.stderr, flush=True)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2512_16473_amd as moe
+    import synth
+
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    torch.cuda.set_device(0)
+    wl = synth.WORKLOADS[args.workload]
+    steps_total = args.warmup + args.steps
+    assert steps_total <= wl.T, f"at most {wl.T} decode steps in this workload"
+    world = build_world(torch, moe, synth, wl, steps_total, args.seed, args.threads)
+    rt, xd = world["rt"], world["xd"]
+    L, k, d = wl.L, wl.k, wl.d
+    out = torch.empty((2, L, d), dtype=torch.float32, device="cuda")
+    streams = (torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream())
+    idx = np.empty((L, k), np.int32)
+    wts = np.empty((L, k), np.float32)
+    hit = np.empty((L, k), np.uint8)
+
+    for t in range(args.warmup):
+        rt.decode_step(xd[t], out[t % 2], streams, idx, wts, hit)
+    torch.cuda.synchronize()
+    rt.sync()
+    rt.reset_stats()
+    rt.set_timing(True)
+
+    torch.cuda.synchronize()
+    rt.sync()
+    t0 = time.perf_counter()
+    for t in range(args.warmup, steps_total):
+        rt.decode_step(xd[t], out[t % 2], streams, idx, wts, hit)
+    torch.cuda.synchronize()
+    rt.sync()
+    t1 = time.perf_counter()
+    st = rt.stats()
+    rt.set_timing(False)
+
+    K = args.steps
+    dt = t1 - t0
+    tok_s = K / dt
+    gu_gbs = st["gate_up_bytes"] / (st["gate_up_ms"] * 1e-3) / 1e9 if st["gate_up_ms"] > 0 else 0.0
+    hit_bytes = st["gate_up_bytes"] + st["down_bytes"]
+    hit_ms = st["gate_up_ms"] + st["down_ms"]
+    sel = st["expert_hits"] + st["expert_misses"]
+    result = {
+        "metric": "decode MoE-layer tokens/s + achieved HBM GB/s (%peak), Mixtral-8x7B shape",
+        "value": round(tok_s, 3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(dt / K * 1e3, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": wl.desc,
+            "d_model": wl.d, "d_ffn": wl.f, "experts": wl.n, "top_k": wl.k, "layers": wl.L,
+            "cache_ways": wl.ways, "shared_d_ffn": wl.f_shared, "batch": 1,
+            "weights": "bf16, fp32 accumulate", "cache_start": f"cold, {args.warmup} warmup tokens",
+            "host_threads": world["hp"].threads, "parallelism": "single GPU",
+        },
+        "roofline": {
+            "kernel": "k_gate_up (W1/W3 rows + SiLU*mul)",
+            "bound": "hbm",
+            "achieved": round(gu_gbs, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(gu_gbs / HBM_PEAK_GBS, 4),
+            "traffic": None,
+            "launches": st["gate_up_launches"],
+            "avg_us": round(st["gate_up_ms"] / max(1, st["gate_up_launches"]) * 1e3, 2),
+            "bytes_per_launch": round(st["gate_up_bytes"] / max(1, st["gate_up_launches"])),
+        },
+        "hit_ffn": {
+            "gbs": round(hit_bytes / (hit_ms * 1e-3) / 1e9, 1) if hit_ms > 0 else 0.0,
+            "frac": round(hit_bytes / (hit_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4) if hit_ms > 0 else 0.0,
+            "down_avg_us": round(st["down_ms"] / max(1, st["down_launches"]) * 1e3, 2),
+            "down_gbs": round(st["down_bytes"] / (st["down_ms"] * 1e-3) / 1e9, 1) if st["down_ms"] > 0 else 0.0,
+            "gpu_us_per_layer": round(hit_ms / max(1, st["gate_up_launches"]) * 1e3, 2),
+        },
+        "trace": {
+            "expert_hit_rate": round(st["expert_hits"] / max(1, sel), 4),
+            "misses_per_token": round(st["expert_misses"] / K, 3),
+            "host_ffn_ms_per_token": round(st["host_ffn_ms"] / K, 3),
+            "route_wait_ms_per_token": round(st["route_wait_ms"] / K, 3),
+            "fills_per_token": round(st["fills"] / K, 3),
+        },
+    }
+    log(json.dumps(result["trace"]), json.dumps(result["hit_ffn"]))
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, world, args.seed, args.cpu_baseline_s, args.warmup)
+    else:
+        result["cpu_baseline"] = None
+    rt.close()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

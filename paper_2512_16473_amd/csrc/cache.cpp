@@ -1,0 +1,164 @@
+// Host-side slot table of the N-index, M-way expert cache (Section III-B):
+// one set per layer, LRU replacement, every missed expert inserted for future
+// tokens (Section III-A step 3).
+#include <algorithm>
+#include <cstring>
+#include <vector>
+
+#include "cache.h"
+#include "common.h"
+
+namespace moe {
+
+bool Cache::valid_selection(const int32_t *experts, int k) const
+{
+    if (k < 1 || k > top_k) return false;
+    for (int a = 0; a < k; ++a) {
+        if (experts[a] < 0 || experts[a] >= n) return false;
+        for (int b = 0; b < a; ++b)
+            if (experts[a] == experts[b]) return false;
+    }
+    return true;
+}
+
+void Cache::reset()
+{
+    std::fill(slot_expert.begin(), slot_expert.end(), -1);
+    std::fill(slot_used.begin(), slot_used.end(), 0);
+    std::fill(tick.begin(), tick.end(), 0);
+    std::fill(where.begin(), where.end(), -1);
+}
+
+void Cache::check(int layer, const int32_t *experts, int k, int32_t *slot_out, uint8_t *hit_out) const
+{
+    const int32_t *map = &where[(size_t)layer * n];
+    for (int j = 0; j < k; ++j) {
+        const int32_t s = map[experts[j]];
+        if (slot_out) slot_out[j] = s;
+        if (hit_out) hit_out[j] = s >= 0 ? 1 : 0;
+    }
+}
+
+void Cache::step(int layer, const int32_t *experts, int k, int32_t *fill_out, int32_t *evicted_out)
+{
+    int32_t *sx = &slot_expert[(size_t)layer * ways];
+    uint64_t *su = &slot_used[(size_t)layer * ways];
+    int32_t *map = &where[(size_t)layer * n];
+    uint64_t &clk = tick[layer];
+
+    // Hit status of every selected expert is fixed before any change.
+    bool hit[MOE_MAX_TOPK];
+    for (int j = 0; j < k; ++j) hit[j] = map[experts[j]] >= 0;
+
+    // Visit the selection in ascending expert id.
+    int order[MOE_MAX_TOPK];
+    for (int j = 0; j < k; ++j) order[j] = j;
+    std::sort(order, order + k, [&](int a, int b) { return experts[a] < experts[b]; });
+
+    for (int q = 0; q < k; ++q) {
+        const int j = order[q];
+        const int32_t e = experts[j];
+        ++clk;
+        if (hit[j]) {
+            su[map[e]] = clk;
+            if (fill_out) fill_out[j] = -1;
+            if (evicted_out) evicted_out[j] = -1;
+            continue;
+        }
+        int victim = -1;
+        for (int s = 0; s < ways; ++s)
+            if (sx[s] < 0) { victim = s; break; }
+        if (victim < 0) {
+            uint64_t oldest = ~(uint64_t)0;
+            for (int s = 0; s < ways; ++s) {
+                bool current = false;
+                for (int c = 0; c < k; ++c)
+                    if (experts[c] == sx[s]) { current = true; break; }
+                if (!current && su[s] < oldest) { oldest = su[s]; victim = s; }
+            }
+        }
+        const int32_t old = sx[victim];
+        if (old >= 0) map[old] = -1;
+        sx[victim] = e;
+        su[victim] = clk;
+        map[e] = victim;
+        if (fill_out) fill_out[j] = victim;
+        if (evicted_out) evicted_out[j] = old;
+    }
+}
+
+}  // namespace moe
+
+using moe::Cache;
+
+extern "C" {
+
+int moe_cache_create(int n_layers, int n_experts, int ways, int top_k, moe_cache **out)
+{
+    MOE_GUARD_BEGIN
+    MOE_REQUIRE(out, "moe_cache_create: null output handle");
+    MOE_REQUIRE(n_layers >= 1, "moe_cache_create: n_layers=%d < 1", n_layers);
+    MOE_REQUIRE(n_experts >= 1 && n_experts <= MOE_MAX_EXPERTS, "moe_cache_create: n_experts=%d out of [1,%d]",
+                n_experts, MOE_MAX_EXPERTS);
+    MOE_REQUIRE(top_k >= 1 && top_k <= MOE_MAX_TOPK, "moe_cache_create: top_k=%d out of [1,%d]", top_k,
+                MOE_MAX_TOPK);
+    MOE_REQUIRE(ways >= top_k && ways <= n_experts,
+                "moe_cache_create: need top_k <= ways <= n_experts (ways=%d top_k=%d n=%d)", ways, top_k,
+                n_experts);
+    Cache *c = new Cache();
+    c->layers = n_layers;
+    c->n = n_experts;
+    c->ways = ways;
+    c->top_k = top_k;
+    c->slot_expert.assign((size_t)n_layers * ways, -1);
+    c->slot_used.assign((size_t)n_layers * ways, 0);
+    c->tick.assign((size_t)n_layers, 0);
+    c->where.assign((size_t)n_layers * n_experts, -1);
+    *out = reinterpret_cast<moe_cache *>(c);
+    return MOE_OK;
+    MOE_GUARD_END
+}
+
+void moe_cache_destroy(moe_cache *c) { delete reinterpret_cast<Cache *>(c); }
+
+int moe_cache_reset(moe_cache *c)
+{
+    MOE_REQUIRE(c, "moe_cache_reset: null handle");
+    reinterpret_cast<Cache *>(c)->reset();
+    return MOE_OK;
+}
+
+int moe_cache_lookup(const moe_cache *ch, int layer, const int32_t *experts, int k, int32_t *slot_out,
+                     uint8_t *hit_out)
+{
+    const Cache *c = reinterpret_cast<const Cache *>(ch);
+    MOE_REQUIRE(c && experts, "moe_cache_lookup: null pointer");
+    MOE_REQUIRE(layer >= 0 && layer < c->layers, "moe_cache_lookup: layer=%d out of [0,%d)", layer, c->layers);
+    MOE_REQUIRE(c->valid_selection(experts, k),
+                "moe_cache_lookup: need 1 <= k <= top_k distinct expert ids in [0,%d)", c->n);
+    c->check(layer, experts, k, slot_out, hit_out);
+    return MOE_OK;
+}
+
+int moe_cache_update(moe_cache *ch, int layer, const int32_t *experts, int k, int32_t *fill_slot_out,
+                     int32_t *evicted_out)
+{
+    Cache *c = reinterpret_cast<Cache *>(ch);
+    MOE_REQUIRE(c && experts, "moe_cache_update: null pointer");
+    MOE_REQUIRE(layer >= 0 && layer < c->layers, "moe_cache_update: layer=%d out of [0,%d)", layer, c->layers);
+    MOE_REQUIRE(c->valid_selection(experts, k),
+                "moe_cache_update: need 1 <= k <= top_k distinct expert ids in [0,%d)", c->n);
+    c->step(layer, experts, k, fill_slot_out, evicted_out);
+    return MOE_OK;
+}
+
+int moe_cache_slotmap(const moe_cache *ch, int layer, int32_t *slotmap_out)
+{
+    const Cache *c = reinterpret_cast<const Cache *>(ch);
+    MOE_REQUIRE(c && slotmap_out, "moe_cache_slotmap: null pointer");
+    MOE_REQUIRE(layer >= 0 && layer < c->layers, "moe_cache_slotmap: layer=%d out of [0,%d)", layer, c->layers);
+    std::memcpy(slotmap_out, &c->where[(size_t)layer * c->n], sizeof(int32_t) * (size_t)c->n);
+    return MOE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,24 @@
+// Host-side expert-cache slot table (one LRU set per layer).
+#pragma once
+
+#include <cstdint>
+#include <vector>
+
+namespace moe {
+
+struct Cache {
+    int layers = 0, n = 0, ways = 0, top_k = 0;
+    std::vector<int32_t> slot_expert;   // [layers][ways], -1 empty
+    std::vector<uint64_t> slot_used;    // [layers][ways], recency tick of the slot
+    std::vector<uint64_t> tick;         // [layers]
+    std::vector<int32_t> where;         // [layers][n], expert -> slot or -1
+
+    bool valid_selection(const int32_t *experts, int k) const;
+    void reset();
+    // Step 1: slot and hit flag of each selected expert (state unchanged).
+    void check(int layer, const int32_t *experts, int k, int32_t *slot_out, uint8_t *hit_out) const;
+    // LRU update for one token; outputs aligned with `experts` (nullable).
+    void step(int layer, const int32_t *experts, int k, int32_t *fill_out, int32_t *evicted_out);
+};
+
+}  // namespace moe

@@ -1,0 +1,70 @@
+// Internal interfaces between the C ABI (host C++) and the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace moe {
+
+constexpr int kMaxJobs = 17;        // up to 16 routed experts + one shared expert
+constexpr int kSegMax = 4096;       // down-projection reduction segment (elements)
+constexpr int kRowsPerDownItem = 16;
+
+// Parameters of the hit-expert FFN (gate/up/SiLU, down, reduce). A "job" is one
+// expert to evaluate: routed job j < k takes its slab from the slot pool at
+// slot = slotmap ? slotmap[sel[j]] : sel[j] (skipped when < 0 or when sel[j] is
+// out of range, or when the slot is outside [0, nslots)); job k is the shared expert when `shared` is non-null.
+struct FfnParams {
+    const float *x;              // [d]
+    const uint8_t *pool;         // slot pool base
+    uint64_t slab_stride;        // bytes between slabs
+    const int32_t *sel;          // [k]
+    const int32_t *slotmap;      // [n] or null
+    const float *w;              // [k] gate weights (applied in the reduce)
+    int k;
+    int n;                       // experts per layer (range check of sel when slotmap is used)
+    int nslots;                  // slabs in the pool; slots outside [0, nslots) are inactive
+    const uint8_t *shared;       // shared-expert slab or null
+    int f_shared;
+    int d, f;
+    int32_t *jobslot;            // [kMaxJobs] slot of each job, -1 inactive (written by gate/up)
+    float *h;                    // [kMaxJobs][hstride]
+    int hstride;
+    float *partial;              // [kMaxJobs][smax][d]
+    int smax;
+};
+
+// Workspace layout helpers.
+size_t ffn_workspace_bytes(int max_jobs, int d, int f_max);
+void ffn_bind_workspace(FfnParams &p, void *ws, int max_jobs, int d, int f_max);
+
+// Events recorded around the two weight-streaming kernels (all null = no timing).
+struct FfnEvents {
+    hipEvent_t start = nullptr, mid = nullptr, end = nullptr;
+};
+
+hipError_t launch_router(const float *x, const float *wr, int T, int d, int n, int k,
+                         int32_t *idx, float *w, hipStream_t s);
+// gate/up/SiLU then down; `after_down` (nullable) is recorded right after the down kernel.
+hipError_t launch_ffn_stream(const FfnParams &p, hipStream_t s, const FfnEvents *ev,
+                             hipEvent_t after_down);
+// out = sum over active jobs of weight * sum of split partials (+ y_extra).
+hipError_t launch_ffn_reduce(const FfnParams &p, const float *y_extra, float *out, hipStream_t s);
+hipError_t launch_combine(const float *a, const float *b, const float *c, int d, float *out,
+                          hipStream_t s);
+
+// Prefill (grouped, MFMA).
+struct PrefillPlan {
+    int d, f, n, k, T;
+    const float *wr;
+    const uint8_t *pool;
+    uint64_t slab_stride;
+};
+size_t prefill_workspace_bytes(int d, int f, int n, int k, int T);
+hipError_t launch_prefill(const PrefillPlan &P, const float *X, float *OUT, int32_t *idx,
+                          float *w, void *ws, hipStream_t s);
+
+int device_cu_count();
+
+}  // namespace moe

@@ -1,0 +1,412 @@
+// One MoE layer of single-request decode, Section III-A of the paper:
+//   step 1  cache check of the selected experts in the layer's set;
+//   step 2a cache hits computed on the GPU from their cache slots;
+//   step 2b the hidden state copied to the host, missed experts computed there;
+//   step 3  missed experts' weights copied into the cache for future tokens
+//           (post-fetch), on a stream of its own (Section III-C keeps weight copies
+//           off the stream that carries activations).
+//
+// Device side, in stream order on the compute stream: [wait for the previous
+// post-fetch into this layer's set] router -> gate/up/SiLU -> down -> [host miss
+// result H2D] -> reduce+combine. The hit kernels resolve expert -> slot on the
+// device from a mirror of the host slot table, so they never wait for the host.
+// The routing and the hidden state are read back on the activation stream while
+// the hit kernels run; the host then updates the LRU table, runs the misses on its
+// thread pool and enqueues the combine. Post-fetched slabs and the updated mirror
+// row land on the copy stream; the next token's use of this layer waits on that
+// copy, so the hit/miss sequence does not depend on timing.
+#include <chrono>
+#include <cstring>
+#include <vector>
+
+#include "cache.h"
+#include "common.h"
+#include "hostpath.h"
+#include "moe_internal.h"
+
+namespace {
+
+struct TimingRec {
+    hipEvent_t start, mid, end;
+    int hits_gate;      // routed jobs resolved as hits are unknown on the host at
+    double bytes_gu;    // launch time; bytes are filled in from the host-side check
+    double bytes_dn;
+};
+
+}  // namespace
+
+struct moe_runtime {
+    moe_layer_desc desc{};
+    std::vector<const void *> host_slabs;   // [L][n]
+    size_t slab_bytes = 0, shared_bytes = 0;
+    size_t slab_payload = 0;                // 3*d*f*2, the bytes a post-fetch copies
+    moe::Cache *cache = nullptr;
+    moe::HostPool *pool = nullptr;
+
+    // device
+    int32_t *d_slotmap = nullptr;   // [L][n]
+    int32_t *d_idx = nullptr;       // [k]
+    float *d_w = nullptr;           // [k]
+    float *d_yhost = nullptr;       // [d]
+    void *d_ws = nullptr;
+    size_t ws_bytes = 0;
+
+    // pinned host staging
+    int32_t *h_idx = nullptr;       // [k]
+    float *h_w = nullptr;           // [k]
+    float *h_x = nullptr;           // [d]
+    float *h_y = nullptr;           // [L][d]
+    int32_t *h_slotmap = nullptr;   // [L][n]
+
+    hipEvent_t ev_router = nullptr, ev_route = nullptr, ev_hits = nullptr;
+    std::vector<hipEvent_t> ev_fill;   // [L]
+    std::vector<char> fill_pending;    // [L]
+
+    bool timing = false;
+    std::vector<TimingRec> pending;    // recorded, not yet resolved
+    std::vector<hipEvent_t> spare;     // resolved events for reuse
+
+    moe_runtime_stats stats{};
+};
+
+namespace {
+
+void release(moe_runtime *rt)
+{
+    if (!rt) return;
+    for (auto &r : rt->pending) {
+        (void)hipEventDestroy(r.start);
+        (void)hipEventDestroy(r.mid);
+        (void)hipEventDestroy(r.end);
+    }
+    for (auto e : rt->spare) (void)hipEventDestroy(e);
+    for (auto e : rt->ev_fill)
+        if (e) (void)hipEventDestroy(e);
+    if (rt->ev_router) (void)hipEventDestroy(rt->ev_router);
+    if (rt->ev_route) (void)hipEventDestroy(rt->ev_route);
+    if (rt->ev_hits) (void)hipEventDestroy(rt->ev_hits);
+    if (rt->d_slotmap) (void)hipFree(rt->d_slotmap);
+    if (rt->d_idx) (void)hipFree(rt->d_idx);
+    if (rt->d_w) (void)hipFree(rt->d_w);
+    if (rt->d_yhost) (void)hipFree(rt->d_yhost);
+    if (rt->d_ws) (void)hipFree(rt->d_ws);
+    if (rt->h_idx) (void)hipHostFree(rt->h_idx);
+    if (rt->h_w) (void)hipHostFree(rt->h_w);
+    if (rt->h_x) (void)hipHostFree(rt->h_x);
+    if (rt->h_y) (void)hipHostFree(rt->h_y);
+    if (rt->h_slotmap) (void)hipHostFree(rt->h_slotmap);
+    delete rt;
+}
+
+hipEvent_t take_event(moe_runtime *rt)
+{
+    if (!rt->spare.empty()) {
+        hipEvent_t e = rt->spare.back();
+        rt->spare.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+// Resolve recorded timing events (the compute stream must have been synchronised).
+int resolve_timing(moe_runtime *rt)
+{
+    for (auto &r : rt->pending) {
+        float a = 0.f, b = 0.f;
+        MOE_HIP(hipEventSynchronize(r.end));
+        MOE_HIP(hipEventElapsedTime(&a, r.start, r.mid));
+        MOE_HIP(hipEventElapsedTime(&b, r.mid, r.end));
+        rt->stats.gate_up_launches += 1;
+        rt->stats.gate_up_ms += a;
+        rt->stats.gate_up_bytes += r.bytes_gu;
+        rt->stats.down_launches += 1;
+        rt->stats.down_ms += b;
+        rt->stats.down_bytes += r.bytes_dn;
+        rt->spare.push_back(r.start);
+        rt->spare.push_back(r.mid);
+        rt->spare.push_back(r.end);
+    }
+    rt->pending.clear();
+    return MOE_OK;
+}
+
+double now_ms()
+{
+    return std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now().time_since_epoch()).count();
+}
+
+}  // namespace
+
+extern "C" {
+
+int moe_runtime_create(const moe_layer_desc *desc, moe_runtime **out)
+{
+    MOE_GUARD_BEGIN
+    MOE_REQUIRE(desc && out, "moe_runtime_create: null pointer");
+    const moe_layer_desc &D = *desc;
+    MOE_REQUIRE(D.d > 0 && D.d % 8 == 0 && D.d <= MOE_MAX_D, "moe_runtime_create: d=%d must be a multiple of 8 in [8,%d]",
+                D.d, MOE_MAX_D);
+    MOE_REQUIRE(D.f > 0 && D.f % 8 == 0, "moe_runtime_create: f=%d must be a positive multiple of 8", D.f);
+    MOE_REQUIRE(D.f_shared >= 0 && D.f_shared % 8 == 0, "moe_runtime_create: f_shared=%d must be a multiple of 8",
+                D.f_shared);
+    MOE_REQUIRE(D.n >= 1 && D.n <= MOE_MAX_EXPERTS, "moe_runtime_create: n=%d out of range", D.n);
+    MOE_REQUIRE(D.k >= 1 && D.k <= MOE_MAX_TOPK && D.k <= D.ways && D.ways <= D.n,
+                "moe_runtime_create: need 1 <= k <= ways <= n (k=%d ways=%d n=%d)", D.k, D.ways, D.n);
+    MOE_REQUIRE(D.n_layers >= 1, "moe_runtime_create: n_layers=%d < 1", D.n_layers);
+    MOE_REQUIRE(D.w_router && D.slot_pool && D.host_slabs && D.cache && D.pool, "moe_runtime_create: null pointer");
+    MOE_REQUIRE(D.f_shared == 0 || D.shared_pool, "moe_runtime_create: f_shared > 0 needs shared_pool");
+    MOE_REQUIRE(moe::aligned16(D.w_router) && moe::aligned16(D.slot_pool) &&
+                    (!D.shared_pool || moe::aligned16(D.shared_pool)),
+                "moe_runtime_create: device pointers must be 16-byte aligned");
+    const moe::Cache *c = reinterpret_cast<const moe::Cache *>(D.cache);
+    MOE_REQUIRE(c->layers == D.n_layers && c->n == D.n && c->ways == D.ways && c->top_k == D.k,
+                "moe_runtime_create: cache geometry (L=%d n=%d ways=%d k=%d) differs from the descriptor",
+                c->layers, c->n, c->ways, c->top_k);
+    const size_t nh = (size_t)D.n_layers * D.n;
+    for (size_t i = 0; i < nh; ++i)
+        MOE_REQUIRE(D.host_slabs[i], "moe_runtime_create: host_slabs[%zu] is null", i);
+
+    moe_runtime *rt = new moe_runtime();
+    rt->desc = D;
+    rt->host_slabs.assign(D.host_slabs, D.host_slabs + nh);
+    rt->desc.host_slabs = rt->host_slabs.data();
+    rt->slab_bytes = moe_slab_bytes(D.d, D.f);
+    rt->slab_payload = (size_t)3 * D.d * D.f * 2;
+    rt->shared_bytes = D.f_shared ? moe_slab_bytes(D.d, D.f_shared) : 0;
+    rt->cache = reinterpret_cast<moe::Cache *>(D.cache);
+    rt->pool = reinterpret_cast<moe::HostPool *>(D.pool);
+
+    auto fail = [&](hipError_t e, const char *what) {
+        moe::set_error("moe_runtime_create: %s failed: %s", what, hipGetErrorString(e));
+        release(rt);
+        return e == hipErrorOutOfMemory ? MOE_ENOMEM : MOE_EHIP;
+    };
+    hipError_t e;
+    const int fmax = D.f > D.f_shared ? D.f : D.f_shared;
+    rt->ws_bytes = moe::ffn_workspace_bytes(D.k + 1, D.d, fmax);
+    if ((e = hipMalloc(&rt->d_ws, rt->ws_bytes)) != hipSuccess) return fail(e, "hipMalloc(workspace)");
+    if ((e = hipMalloc((void **)&rt->d_slotmap, sizeof(int32_t) * nh)) != hipSuccess) return fail(e, "hipMalloc");
+    if ((e = hipMalloc((void **)&rt->d_idx, sizeof(int32_t) * D.k)) != hipSuccess) return fail(e, "hipMalloc");
+    if ((e = hipMalloc((void **)&rt->d_w, sizeof(float) * D.k)) != hipSuccess) return fail(e, "hipMalloc");
+    if ((e = hipMalloc((void **)&rt->d_yhost, sizeof(float) * D.d)) != hipSuccess) return fail(e, "hipMalloc");
+    if ((e = hipHostMalloc((void **)&rt->h_idx, sizeof(int32_t) * D.k, 0)) != hipSuccess) return fail(e, "hipHostMalloc");
+    if ((e = hipHostMalloc((void **)&rt->h_w, sizeof(float) * D.k, 0)) != hipSuccess) return fail(e, "hipHostMalloc");
+    if ((e = hipHostMalloc((void **)&rt->h_x, sizeof(float) * D.d, 0)) != hipSuccess) return fail(e, "hipHostMalloc");
+    if ((e = hipHostMalloc((void **)&rt->h_y, sizeof(float) * D.d * (size_t)D.n_layers, 0)) != hipSuccess)
+        return fail(e, "hipHostMalloc");
+    if ((e = hipHostMalloc((void **)&rt->h_slotmap, sizeof(int32_t) * nh, 0)) != hipSuccess)
+        return fail(e, "hipHostMalloc");
+    // Mirror of the host table as it stands now.
+    for (int l = 0; l < D.n_layers; ++l)
+        std::memcpy(rt->h_slotmap + (size_t)l * D.n, &c->where[(size_t)l * D.n], sizeof(int32_t) * D.n);
+    if ((e = hipMemcpy(rt->d_slotmap, rt->h_slotmap, sizeof(int32_t) * nh, hipMemcpyHostToDevice)) != hipSuccess)
+        return fail(e, "hipMemcpy(slotmap)");
+    if ((e = hipEventCreateWithFlags(&rt->ev_router, hipEventDisableTiming)) != hipSuccess) return fail(e, "event");
+    if ((e = hipEventCreateWithFlags(&rt->ev_route, hipEventDisableTiming)) != hipSuccess) return fail(e, "event");
+    if ((e = hipEventCreateWithFlags(&rt->ev_hits, hipEventDisableTiming)) != hipSuccess) return fail(e, "event");
+    rt->ev_fill.assign(D.n_layers, nullptr);
+    rt->fill_pending.assign(D.n_layers, 0);
+    for (int l = 0; l < D.n_layers; ++l)
+        if ((e = hipEventCreateWithFlags(&rt->ev_fill[l], hipEventDisableTiming)) != hipSuccess)
+            return fail(e, "event");
+    *out = rt;
+    return MOE_OK;
+    MOE_GUARD_END
+}
+
+void moe_runtime_destroy(moe_runtime *rt)
+{
+    if (!rt) return;
+    (void)hipDeviceSynchronize();
+    release(rt);
+}
+
+int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out_dev, int32_t *idx_host,
+                      float *w_host, uint8_t *hit_host, void *compute_stream, void *act_stream, void *copy_stream)
+{
+    MOE_GUARD_BEGIN
+    MOE_REQUIRE(rt && x_dev && out_dev, "moe_layer_forward: null pointer");
+    const moe_layer_desc &D = rt->desc;
+    MOE_REQUIRE(layer >= 0 && layer < D.n_layers, "moe_layer_forward: layer=%d out of [0,%d)", layer, D.n_layers);
+    MOE_REQUIRE(moe::aligned16(x_dev) && moe::aligned16(out_dev), "moe_layer_forward: x/out not 16-byte aligned");
+    hipStream_t sc = (hipStream_t)compute_stream, sa = (hipStream_t)act_stream, sw = (hipStream_t)copy_stream;
+    const int d = D.d, n = D.n, k = D.k;
+
+    // The previous post-fetch into this set (slabs and mirror row) must be complete
+    // before this token routes through the layer.
+    if (rt->fill_pending[layer]) MOE_HIP(hipStreamWaitEvent(sc, rt->ev_fill[layer], 0));
+
+    // Router on the compute stream; read-back of routing and hidden state on the
+    // activation stream.
+    const float *wr = D.w_router + (size_t)layer * n * d;
+    MOE_HIP(moe::launch_router(x_dev, wr, 1, d, n, k, rt->d_idx, rt->d_w, sc));
+    MOE_HIP(hipEventRecord(rt->ev_router, sc));
+    MOE_HIP(hipStreamWaitEvent(sa, rt->ev_router, 0));
+    MOE_HIP(hipMemcpyAsync(rt->h_idx, rt->d_idx, sizeof(int32_t) * k, hipMemcpyDeviceToHost, sa));
+    MOE_HIP(hipMemcpyAsync(rt->h_w, rt->d_w, sizeof(float) * k, hipMemcpyDeviceToHost, sa));
+    MOE_HIP(hipMemcpyAsync(rt->h_x, x_dev, sizeof(float) * d, hipMemcpyDeviceToHost, sa));
+    MOE_HIP(hipEventRecord(rt->ev_route, sa));
+
+    // Hit experts on the device (slots from the device mirror of the table).
+    moe::FfnParams p{};
+    p.x = x_dev;
+    p.pool = static_cast<const uint8_t *>(D.slot_pool) + (size_t)layer * D.ways * rt->slab_bytes;
+    p.slab_stride = rt->slab_bytes;
+    p.sel = rt->d_idx;
+    p.slotmap = rt->d_slotmap + (size_t)layer * n;
+    p.w = rt->d_w;
+    p.k = k;
+    p.n = n;
+    p.nslots = D.ways;
+    p.shared = D.f_shared ? static_cast<const uint8_t *>(D.shared_pool) + (size_t)layer * rt->shared_bytes : nullptr;
+    p.f_shared = D.f_shared;
+    p.d = d;
+    p.f = D.f;
+    moe::ffn_bind_workspace(p, rt->d_ws, k + 1, d, D.f > D.f_shared ? D.f : D.f_shared);
+    moe::FfnEvents ev;
+    TimingRec rec{};
+    if (rt->timing) {
+        rec.start = take_event(rt);
+        rec.mid = take_event(rt);
+        rec.end = take_event(rt);
+        MOE_REQUIRE(rec.start && rec.mid && rec.end, "moe_layer_forward: could not create timing events");
+        ev.start = rec.start;
+        ev.mid = rec.mid;
+        ev.end = rec.end;
+    }
+    MOE_HIP(moe::launch_ffn_stream(p, sc, rt->timing ? &ev : nullptr, rt->ev_hits));
+
+    // Step 1 on the host: the routing read-back, then check + LRU update.
+    const double t0 = now_ms();
+    MOE_HIP(hipEventSynchronize(rt->ev_route));
+    const double t1 = now_ms();
+    rt->stats.route_wait_ms += t1 - t0;
+    int32_t sel[MOE_MAX_TOPK], fill[MOE_MAX_TOPK], evicted[MOE_MAX_TOPK];
+    float wsel[MOE_MAX_TOPK];
+    uint8_t hit[MOE_MAX_TOPK];
+    std::memcpy(sel, rt->h_idx, sizeof(int32_t) * k);
+    std::memcpy(wsel, rt->h_w, sizeof(float) * k);
+    MOE_REQUIRE(rt->cache->valid_selection(sel, k), "moe_layer_forward: router returned an invalid selection");
+    rt->cache->check(layer, sel, k, nullptr, hit);
+    rt->cache->step(layer, sel, k, fill, evicted);
+
+    int nmiss = 0, nhit = 0;
+    const void *mslab[MOE_MAX_TOPK];
+    float mw[MOE_MAX_TOPK];
+    for (int j = 0; j < k; ++j) {
+        if (hit[j]) { ++nhit; continue; }
+        mslab[nmiss] = rt->host_slabs[(size_t)layer * n + sel[j]];
+        mw[nmiss] = wsel[j];
+        ++nmiss;
+    }
+    if (rt->timing) {
+        const double dd = d, ff = D.f, fs = D.f_shared;
+        rec.bytes_gu = nhit * (2.0 * ff * dd * 2.0 + ff * 4.0) + (fs > 0 ? 2.0 * fs * dd * 2.0 + fs * 4.0 : 0.0) + dd * 4.0;
+        rec.bytes_dn = nhit * (dd * ff * 2.0 + ff * 4.0 + dd * 4.0) + (fs > 0 ? dd * fs * 2.0 + fs * 4.0 + dd * 4.0 : 0.0);
+        rt->pending.push_back(rec);
+    }
+
+    // Step 2(b): misses on the host thread pool, result copied in for the combine.
+    float *yh = rt->h_y + (size_t)layer * d;
+    if (nmiss) {
+        const double t2 = now_ms();
+        rt->pool->expert_ffn(rt->h_x, mslab, mw, nmiss, d, D.f, yh);
+        rt->stats.host_ffn_ms += now_ms() - t2;
+        MOE_HIP(hipMemcpyAsync(rt->d_yhost, yh, sizeof(float) * d, hipMemcpyHostToDevice, sc));
+    }
+    MOE_HIP(moe::launch_ffn_reduce(p, nmiss ? rt->d_yhost : nullptr, out_dev, sc));
+
+    // Step 3: post-fetch of the missed experts into their victim slots. The slabs
+    // can land at once (no current-token expert is ever a victim and the previous
+    // token's kernels on this layer finished before this token's router); the mirror
+    // row is rewritten only after this token's hit kernels have read it.
+    if (nmiss) {
+        uint8_t *set_base = static_cast<uint8_t *>(D.slot_pool) + (size_t)layer * D.ways * rt->slab_bytes;
+        for (int j = 0; j < k; ++j) {
+            if (hit[j]) continue;
+            MOE_HIP(hipMemcpyAsync(set_base + (size_t)fill[j] * rt->slab_bytes,
+                                   rt->host_slabs[(size_t)layer * n + sel[j]], rt->slab_payload,
+                                   hipMemcpyHostToDevice, sw));
+            rt->stats.fills += 1;
+        }
+        int32_t *row = rt->h_slotmap + (size_t)layer * n;
+        std::memcpy(row, &rt->cache->where[(size_t)layer * n], sizeof(int32_t) * n);
+        MOE_HIP(hipStreamWaitEvent(sw, rt->ev_hits, 0));
+        MOE_HIP(hipMemcpyAsync(rt->d_slotmap + (size_t)layer * n, row, sizeof(int32_t) * n, hipMemcpyHostToDevice, sw));
+        MOE_HIP(hipEventRecord(rt->ev_fill[layer], sw));
+        rt->fill_pending[layer] = 1;
+    }
+
+    rt->stats.layer_calls += 1;
+    rt->stats.expert_hits += nhit;
+    rt->stats.expert_misses += nmiss;
+    if (idx_host) std::memcpy(idx_host, sel, sizeof(int32_t) * k);
+    if (w_host) std::memcpy(w_host, wsel, sizeof(float) * k);
+    if (hit_host) std::memcpy(hit_host, hit, k);
+    return MOE_OK;
+    MOE_GUARD_END
+}
+
+int moe_decode_step(moe_runtime *rt, const float *x_dev, float *out_dev, int32_t *idx_host, float *w_host,
+                    uint8_t *hit_host, void *compute_stream, void *act_stream, void *copy_stream)
+{
+    MOE_REQUIRE(rt && x_dev && out_dev, "moe_decode_step: null pointer");
+    const moe_layer_desc &D = rt->desc;
+    for (int l = 0; l < D.n_layers; ++l) {
+        const size_t o = (size_t)l * D.d, q = (size_t)l * D.k;
+        const int rc = moe_layer_forward(rt, l, x_dev + o, out_dev + o, idx_host ? idx_host + q : nullptr,
+                                         w_host ? w_host + q : nullptr, hit_host ? hit_host + q : nullptr,
+                                         compute_stream, act_stream, copy_stream);
+        if (rc != MOE_OK) return rc;
+    }
+    return MOE_OK;
+}
+
+int moe_runtime_sync(moe_runtime *rt)
+{
+    MOE_REQUIRE(rt, "moe_runtime_sync: null handle");
+    for (int l = 0; l < rt->desc.n_layers; ++l)
+        if (rt->fill_pending[l]) MOE_HIP(hipEventSynchronize(rt->ev_fill[l]));
+    return MOE_OK;
+}
+
+int moe_runtime_device_slotmap(moe_runtime *rt, int layer, int32_t *slotmap_out)
+{
+    MOE_REQUIRE(rt && slotmap_out, "moe_runtime_device_slotmap: null pointer");
+    MOE_REQUIRE(layer >= 0 && layer < rt->desc.n_layers, "moe_runtime_device_slotmap: layer out of range");
+    if (rt->fill_pending[layer]) MOE_HIP(hipEventSynchronize(rt->ev_fill[layer]));
+    MOE_HIP(hipMemcpy(slotmap_out, rt->d_slotmap + (size_t)layer * rt->desc.n, sizeof(int32_t) * rt->desc.n,
+                      hipMemcpyDeviceToHost));
+    return MOE_OK;
+}
+
+int moe_runtime_set_timing(moe_runtime *rt, int enable)
+{
+    MOE_REQUIRE(rt, "moe_runtime_set_timing: null handle");
+    const int rc = resolve_timing(rt);
+    if (rc != MOE_OK) return rc;
+    rt->timing = enable != 0;
+    return MOE_OK;
+}
+
+int moe_runtime_get_stats(moe_runtime *rt, moe_runtime_stats *out)
+{
+    MOE_REQUIRE(rt && out, "moe_runtime_get_stats: null pointer");
+    const int rc = resolve_timing(rt);
+    if (rc != MOE_OK) return rc;
+    *out = rt->stats;
+    return MOE_OK;
+}
+
+int moe_runtime_reset_stats(moe_runtime *rt)
+{
+    MOE_REQUIRE(rt, "moe_runtime_reset_stats: null handle");
+    const int rc = resolve_timing(rt);
+    if (rc != MOE_OK) return rc;
+    rt->stats = moe_runtime_stats{};
+    return MOE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,158 @@
+"""C-ABI library checks that need no GPU: symbols, argument validation, and the
+host-side parts of the path (LRU slot table, host expert path) against the oracle."""
+import ctypes
+import itertools
+import random
+import re
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import lru as olru
+import synth
+
+import paper_2512_16473_amd as moe  # noqa: E402
+from paper_2512_16473_amd import _abi  # noqa: E402
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "moe.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(moe_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared_functions()
+    assert len(names) >= 25
+    lib = ctypes.CDLL(_abi.LIB_PATH)
+    for name in names:
+        assert hasattr(lib, name), name
+    assert {s[0] for s in _abi.SIGNATURES} == set(names)
+
+
+def test_version_and_sizes():
+    lib = moe.lib()
+    assert lib.moe_version() >= 100
+    assert moe.slab_bytes(4096, 14336) == 352_321_536
+    assert moe.slab_bytes(256, 512) % 256 == 0 and moe.slab_bytes(256, 512) >= 3 * 256 * 512 * 2
+    assert moe.slab_bytes(0, 8) == 0
+
+
+def test_argument_errors_do_not_touch_the_device():
+    lib = moe.lib()
+    # k > n, n too large, d not a multiple of 8: rejected before any HIP call
+    assert lib.moe_router_topk(None, None, 1, 64, 4, 5, None, None, None) == _abi.MOE_EINVAL
+    assert b"k=5" in lib.moe_last_error()
+    assert lib.moe_router_topk(None, None, 1, 64, 300, 2, None, None, None) == _abi.MOE_EINVAL
+    assert lib.moe_router_topk(None, None, 1, 60, 8, 2, None, None, None) == _abi.MOE_EINVAL
+    assert lib.moe_router_topk(None, None, 0, 64, 8, 2, None, None, None) == _abi.MOE_OK   # T == 0: no-op
+    assert lib.moe_expert_ffn_hits(None, None, 4, None, None, 2, 64, 64, None, None, 0, None) == _abi.MOE_EINVAL
+    assert lib.moe_expert_ffn_hits(None, None, 4, None, None, 17, 64, 64, None, None, 0, None) == _abi.MOE_EINVAL
+    assert lib.moe_combine(None, None, None, 16, None, None) == _abi.MOE_EINVAL
+    assert lib.moe_runtime_create(None, None) == _abi.MOE_EINVAL
+
+
+def test_cache_create_validation():
+    with pytest.raises(moe.MoeError):
+        moe.Cache(2, 8, 1, 2)          # ways < top_k
+    with pytest.raises(moe.MoeError):
+        moe.Cache(2, 8, 9, 2)          # ways > n
+    with pytest.raises(moe.MoeError):
+        moe.Cache(0, 8, 4, 2)
+    c = moe.Cache(2, 8, 4, 2)
+    with pytest.raises(moe.MoeError):
+        c.update(0, [1, 1])            # duplicate ids
+    with pytest.raises(moe.MoeError):
+        c.update(2, [1, 2])            # layer out of range
+    with pytest.raises(moe.MoeError):
+        c.update(0, [1, 8])            # id out of range
+    with pytest.raises(moe.MoeError):
+        c.update(0, [1, 2, 3])         # more than top_k
+    assert np.all(c.slotmap(0) == -1)  # failed calls changed nothing
+
+
+def _lib_trace(seq, n, ways, k):
+    c = moe.Cache(1, n, ways, k)
+    out = []
+    for sel in seq:
+        slots, hits = c.lookup(0, sel)
+        fill, ev = c.update(0, sel)
+        out.append((list(slots), list(hits), list(fill), list(ev)))
+    return out, c
+
+
+@pytest.mark.parametrize("k,ways,length", [(1, 2, 6), (1, 3, 6), (2, 2, 5), (2, 3, 5), (2, 4, 4)])
+def test_library_lru_exhaustive_vs_oracle(k, ways, length):
+    n = 4
+    subs = [list(c) for c in itertools.combinations(range(n), k)]
+    rng = random.Random(ways * 7 + k)
+    c = moe.Cache(1, n, ways, k)
+    for seq in itertools.product(subs, repeat=length):
+        seq = [rng.sample(s, len(s)) for s in seq]
+        c.reset()
+        ref = olru.LRUSet(ways)
+        for sel in seq:
+            slots, hits = c.lookup(0, sel)
+            fill, ev = c.update(0, sel)
+            r_slots, r_hits, r_fill, r_ev = ref.access(sel)
+            assert list(slots) == r_slots and list(hits) == r_hits
+            assert list(fill) == r_fill and list(ev) == r_ev
+
+
+@pytest.mark.parametrize("n,k,ways", [(8, 2, 4), (16, 2, 6), (64, 8, 24)])
+def test_library_lru_long_traces_vs_oracle(n, k, ways):
+    rng = random.Random(n + ways)
+    L = 3
+    c = moe.Cache(L, n, ways, k)
+    ref = olru.LRUCache(L, ways)
+    # correlated selections (a mix of reuse and fresh draws), several layers interleaved
+    prev = [rng.sample(range(n), k) for _ in range(L)]
+    for t in range(600):
+        for layer in range(L):
+            keep = [e for e in prev[layer] if rng.random() < 0.6]
+            fresh = [e for e in rng.sample(range(n), n) if e not in keep][: k - len(keep)]
+            sel = keep + fresh
+            rng.shuffle(sel)
+            prev[layer] = sel
+            slots, hits = c.lookup(layer, sel)
+            fill, ev = c.update(layer, sel)
+            r = ref.access(layer, sel)
+            assert (list(slots), list(hits), list(fill), list(ev)) == r
+            assert list(c.slotmap(layer)) == ref.slotmap(layer, n)
+
+
+def _pool_case(d, f, ne, seed):
+    slabs = [synth.expert_slab(seed + j, d, f, None) for j in range(ne)]
+    rng = np.random.default_rng(seed)
+    x = rng.standard_normal(d).astype(np.float32)
+    w = rng.random(ne).astype(np.float32)
+    w /= w.sum()
+    return x, slabs, w
+
+
+@pytest.mark.parametrize("d,f,ne", [(256, 512, 2), (64, 40, 3), (512, 1024, 1), (128, 96, 8)])
+def test_host_expert_path_vs_oracle(d, f, ne):
+    x, slabs, w = _pool_case(d, f, ne, 40 + d + ne)
+    pool = moe.HostPool(4)
+    y = pool.expert_ffn(x, slabs, w, d, f)
+    ys = np.stack([oracle.expert(x, s, d, f) for s in slabs])
+    ref = oracle.combine(ys, w)
+    rms = float(np.sqrt(np.mean(ref.astype(np.float64) ** 2)))
+    err = float(np.max(np.abs(y - ref)))
+    assert err <= 1e-4 * rms, (err, rms)
+
+
+def test_host_expert_path_thread_independent_and_empty():
+    d, f = 256, 512
+    x, slabs, w = _pool_case(d, f, 2, 5)
+    y1 = moe.HostPool(1).expert_ffn(x, slabs, w, d, f)
+    y5 = moe.HostPool(5).expert_ffn(x, slabs, w, d, f)
+    assert np.array_equal(y1, y5)
+    y0 = moe.HostPool(3).expert_ffn(x, [], np.zeros(0, np.float32), d, f, y=np.full(d, 7.0, np.float32))
+    assert np.all(y0 == 0)
+    with pytest.raises(moe.MoeError):
+        moe.HostPool(2).expert_ffn(x, slabs, w, 250, f)

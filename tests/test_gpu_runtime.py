@@ -1,0 +1,129 @@
+"""The whole per-layer decode path (router, cache check/update, hit FFN on the GPU,
+misses on the host, post-fetch, combine) vs the oracle: routing bit-exact (near-tie
+protocol), hit/miss trace and slot table bit-exact against the oracle LRU replayed on
+the chosen expert sets, outputs within 2e-2 x RMS."""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import lru as olru
+import synth
+from _gpu_util import assert_close, make_slabs_host, router_parity, say, torch_cuda
+
+pytestmark = pytest.mark.gpu
+
+
+class World:
+    """A decode world on the GPU: router weights, slot pool, pinned host experts,
+    shared experts, AR(1) hidden states, library runtime."""
+
+    def __init__(self, name, L=None, T=None, ways=None, threads=4, seed=0):
+        torch = torch_cuda()
+        import paper_2512_16473_amd as moe
+        wl = synth.WORKLOADS[name]
+        self.wl = wl
+        self.L = L or wl.L
+        self.T = T or wl.T
+        self.ways = ways or wl.ways
+        d, f, n, k = wl.d, wl.f, wl.n, wl.k
+        self.d, self.f, self.n, self.k = d, f, n, k
+        self.wr = np.stack([synth.router_weights(synth.seed_for(seed, name, "router", l), n, d)
+                            for l in range(self.L)])
+        self.X = np.stack([synth.ar1_states(synth.seed_for(seed, name, "states", l), self.T, d)
+                           for l in range(self.L)])                       # [L, T, d]
+        self.host, stride, self.views = make_slabs_host(torch, self.L, n, d, f, wl.w_std, seed, name)
+        self.host_addrs = [self.host.ptr + i * stride for i in range(self.L * n)]
+        self.pool = torch.zeros(self.L * self.ways * stride, dtype=torch.uint8, device="cuda")
+        self.shared = None
+        self.shared_views = None
+        if wl.f_shared:
+            sh_host, sstride, self.shared_views = make_slabs_host(torch, self.L, 1, d, wl.f_shared, wl.w_std, seed,
+                                                                  name, kind="shared")
+            self.shared = torch.from_numpy(sh_host.array).cuda()
+            self._sh_host = sh_host
+        self.cache = moe.Cache(self.L, n, self.ways, k)
+        self.hpool = moe.HostPool(threads)
+        self.rt = moe.Runtime(d, f, n, k, self.ways, self.L, torch.from_numpy(self.wr).cuda(), self.pool,
+                              self.host_addrs, self.cache, self.hpool, f_shared=wl.f_shared,
+                              shared_pool=self.shared)
+        self.streams = (torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream())
+        self.xd = torch.from_numpy(np.ascontiguousarray(self.X.transpose(1, 0, 2))).cuda()   # [T, L, d]
+        self.out = torch.empty((self.T, self.L, d), dtype=torch.float32, device="cuda")
+
+    def run(self, steps):
+        idx = np.empty((steps, self.L, self.k), np.int32)
+        w = np.empty((steps, self.L, self.k), np.float32)
+        hit = np.empty((steps, self.L, self.k), np.uint8)
+        for t in range(steps):
+            self.rt.decode_step(self.xd[t], self.out[t], self.streams, idx[t], w[t], hit[t])
+        import torch
+        torch.cuda.synchronize()
+        self.rt.sync()
+        return idx, w, hit.astype(bool), self.out[:steps].cpu().numpy()
+
+    def oracle_out(self, layer, t, expert_set):
+        slabs = self.views[layer * self.n:(layer + 1) * self.n]
+        sh = None if self.shared_views is None else self.shared_views[layer]
+        _, _, out, _ = oracle.moe_token(self.X[layer, t], self.wr[layer], slabs, self.k, self.f,
+                                        shared_slab=sh, f_shared=self.wl.f_shared, forced_set=expert_set)
+        return out
+
+
+def _check_trace(world, idx, w, hit, out, steps, layers, check_out):
+    ref = olru.LRUCache(world.L, world.ways)
+    worst = 0.0
+    for t in range(steps):
+        for l in range(world.L):
+            if l in layers:
+                oidx, ow = router_parity(idx[t, l], w[t, l], world.X[l, t], world.wr[l], world.k)
+            slots, hits, fills, ev = ref.access(l, list(idx[t, l]))
+            assert list(hit[t, l]) == hits, (t, l, list(hit[t, l]), hits)
+            if l in layers and check_out(t, l):
+                o = world.oracle_out(l, t, oidx)
+                worst = max(worst, assert_close(out[t, l], o, f"t={t} layer={l}"))
+    for l in range(world.L):
+        assert list(world.rt.device_slotmap(l)) == ref.slotmap(l, world.n)
+        assert list(world.cache.slotmap(l)) == ref.slotmap(l, world.n)
+    return worst
+
+
+def test_runtime_tiny_full_trace():
+    say("runtime tiny full trace")
+    world = World("tiny")
+    steps = world.T
+    idx, w, hit, out = world.run(steps)
+    worst = _check_trace(world, idx, w, hit, out, steps, set(range(world.L)), lambda t, l: True)
+    st = world.rt.stats()
+    assert st["expert_hits"] + st["expert_misses"] == steps * world.L * world.k
+    assert st["fills"] == st["expert_misses"]
+    assert 0 < st["expert_hits"] and 0 < st["expert_misses"]
+    say("  worst max|err|/RMS", worst, "hit rate", st["expert_hits"] / (steps * world.k))
+
+
+def test_runtime_tiny_all_resident_and_host_only_agree():
+    """The cache changes where experts run, not what they compute (Section I, 'without
+    accuracy trade-offs'): M = n (all hits after warm-up) vs M = k."""
+    say("runtime tiny M=n vs M=k")
+    a = World("tiny", ways=4, T=24)
+    b = World("tiny", ways=2, T=24)
+    ia, wa, ha, oa = a.run(24)
+    ib, wb, hb, ob = b.run(24)
+    assert np.array_equal(ia, ib)
+    assert ha[4:].sum() > hb[4:].sum()
+    for t in range(24):
+        assert_close(oa[t, 0], ob[t, 0], f"t={t}")
+
+
+@pytest.mark.parametrize("name,L,T,layers", [("mixtral", 2, 10, {0, 1}), ("phi", 1, 12, {0}),
+                                             ("fine", 1, 8, {0})])
+def test_runtime_full_shapes(name, L, T, layers):
+    """Full per-layer shapes; fewer layers and steps than the benchmark (host memory
+    and oracle time), same kernels and launch configuration."""
+    oracle.set_threads(min(16, os.cpu_count() or 1))
+    say("runtime", name, "L", L, "T", T)
+    world = World(name, L=L, T=T, threads=8)
+    idx, w, hit, out = world.run(T)
+    worst = _check_trace(world, idx, w, hit, out, T, layers, lambda t, l: t % 3 == 0 or t == T - 1)
+    say("  worst max|err|/RMS", worst)
