@@ -6,7 +6,7 @@ cache check + LRU update, SwiGLU FFN of cache-hit experts on the GPU, missed exp
 on the host thread pool, post-fetch of missed experts into the cache, weighted
 combine (Section III-A steps 1-3). Inputs (router weights, expert weights, AR(1)
 hidden states) are synthetic and seeded; expert weights live in pinned host memory
-(the full model) and in the per-layer GPU expert cache (M of n experts per layer),
+(see build_world for the page-locked cap) and in the per-layer GPU expert cache (M of n experts per layer),
 starting cold. The warmup steps fill the cache; the timed steps run the real LRU
 trace, so they include host-side misses and post-fetch copies.
 
@@ -32,22 +32,31 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def build_world(torch, moe, synth, wl, steps_total, seed, threads):
+def build_world(torch, moe, synth, wl, steps_total, seed, threads, pinned_gb):
+    """Device cache, pinned host experts, router weights and hidden states.
+
+    Page-locked host memory is capped per process on the GPU hosts (64 GiB), below
+    the full Mixtral/Phi/fine-grained expert sets (80-111 GB). The host copies of the
+    experts therefore cover the first H layers, H = floor(pinned_gb / per-layer bytes),
+    and layer l uses host layer l mod H (its router and its cache slots stay its own).
+    """
     import numpy as np
     d, f, n, k, L, M = wl.d, wl.f, wl.n, wl.k, wl.L, wl.ways
     stride = moe.slab_bytes(d, f)
+    per_layer = n * stride
+    H = max(1, min(L, int(pinned_gb * 2**30) // per_layer))
     t0 = time.perf_counter()
-    host = moe.PinnedBuffer(L * n * stride)
-    log(f"pinned host experts: {L * n * stride / 1e9:.1f} GB in {time.perf_counter() - t0:.1f}s")
-    hview = torch.from_numpy(host.array)
+    hosts = [moe.PinnedBuffer(per_layer) for _ in range(H)]
+    log(f"pinned host experts: {H} distinct layers x {per_layer / 1e9:.2f} GB in {time.perf_counter() - t0:.1f}s")
     tmp = torch.empty(3 * d * f, dtype=torch.bfloat16, device="cuda")
-    for l in range(L):
+    for h in range(H):
+        hview = torch.from_numpy(hosts[h].array)
         for e in range(n):
-            synth.expert_slab_torch(synth.seed_for(seed, wl.name, "expert", l, e), d, f, wl.w_std, out=tmp)
-            off = (l * n + e) * stride
-            hview[off: off + 3 * d * f * 2].copy_(tmp.view(torch.uint8))
+            synth.expert_slab_torch(synth.seed_for(seed, wl.name, "expert", h, e), d, f, wl.w_std, out=tmp)
+            hview[e * stride: e * stride + 3 * d * f * 2].copy_(tmp.view(torch.uint8))
     del tmp
     log(f"expert weights drawn: {time.perf_counter() - t0:.1f}s")
+    host_addrs = [hosts[l % H].ptr + e * stride for l in range(L) for e in range(n)]
     shared = None
     if wl.f_shared:
         sstride = moe.slab_bytes(d, wl.f_shared)
@@ -62,11 +71,11 @@ def build_world(torch, moe, synth, wl, steps_total, seed, threads):
     pool = torch.zeros(L * M * stride, dtype=torch.uint8, device="cuda")
     cache = moe.Cache(L, n, M, k)
     hp = moe.HostPool(threads)
-    rt = moe.Runtime(d, f, n, k, M, L, wr, pool, [host.ptr + i * stride for i in range(L * n)], cache, hp,
-                     f_shared=wl.f_shared, shared_pool=shared)
+    rt = moe.Runtime(d, f, n, k, M, L, wr, pool, host_addrs, cache, hp, f_shared=wl.f_shared, shared_pool=shared)
     torch.cuda.synchronize()
     log(f"world ready in {time.perf_counter() - t0:.1f}s (device cache {pool.numel() / 1e9:.1f} GB)")
-    return dict(host=host, wr=wr, X=X, xd=xd, pool=pool, shared=shared, cache=cache, hp=hp, rt=rt, stride=stride)
+    return dict(hosts=hosts, H=H, wr=wr, X=X, xd=xd, pool=pool, shared=shared, cache=cache, hp=hp, rt=rt,
+                stride=stride)
 
 
 def cpu_baseline(wl, world, seed, budget_s, t_first):
@@ -78,7 +87,7 @@ def cpu_baseline(wl, world, seed, budget_s, t_first):
     from oracle import lru as olru
     wr = world["wr"].cpu().numpy()
     X = world["X"]
-    host, stride = world["host"], world["stride"]
+    hosts, H, stride = world["hosts"], world["H"], world["stride"]
     d, f, n, k, L = wl.d, wl.f, wl.n, wl.k, wl.L
     shared_np = None
     if wl.f_shared:
@@ -91,8 +100,7 @@ def cpu_baseline(wl, world, seed, budget_s, t_first):
     order = [(l, t) for l in range(L) for t in range(t_first, T)]
     cache = olru.LRUCache(L, wl.ways)
     for (l, t) in order:
-        slabs = [host.array[(l * n + e) * stride:(l * n + e) * stride + 3 * d * f * 2].view(np.uint16)
-                 for e in range(n)]
+        slabs = [hosts[l % H].array[e * stride:e * stride + 3 * d * f * 2].view(np.uint16) for e in range(n)]
         sh = None
         if shared_np is not None:
             sh = shared_np[l * sstride: l * sstride + 3 * d * wl.f_shared * 2].view(np.uint16)
@@ -127,6 +135,7 @@ def main():
     ap.add_argument("--workload", default="mixtral", choices=["mixtral", "phi", "fine", "tiny"])
     ap.add_argument("--threads", type=int, default=0, help="host expert threads (0: OMP_NUM_THREADS or all cores)")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--pinned-gb", type=float, default=56.0, help="page-locked host memory for expert copies (GiB)")
     ap.add_argument("--cpu-baseline-s", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     args = ap.parse_args()
@@ -145,7 +154,7 @@ def main():
     wl = synth.WORKLOADS[args.workload]
     steps_total = args.warmup + args.steps
     assert steps_total <= wl.T, f"at most {wl.T} decode steps in this workload"
-    world = build_world(torch, moe, synth, wl, steps_total, args.seed, args.threads)
+    world = build_world(torch, moe, synth, wl, steps_total, args.seed, args.threads, args.pinned_gb)
     rt, xd = world["rt"], world["xd"]
     L, k, d = wl.L, wl.k, wl.d
     out = torch.empty((2, L, d), dtype=torch.float32, device="cuda")
@@ -198,6 +207,7 @@ def main():
             "cache_ways": wl.ways, "shared_d_ffn": wl.f_shared, "batch": 1,
             "weights": "bf16, fp32 accumulate", "cache_start": f"cold, {args.warmup} warmup tokens",
             "host_threads": world["hp"].threads, "parallelism": "single GPU",
+            "host_expert_layers_distinct": world["H"],
         },
         "roofline": {
             "kernel": "k_gate_up (W1/W3 rows + SiLU*mul)",
