@@ -122,6 +122,21 @@ def cpu_baseline(wl, world, seed, budget_s, t_first):
     }
 
 
+def measured_traffic(args):
+    """HBM bytes per k_gate_up launch from the committed PMC record, if it was taken on
+    the current kernel source and the same workload arguments; else None."""
+    import hashlib
+    try:
+        rec = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))
+        src = open(os.path.join(ROOT, rec["kernel_source"]), "rb").read()
+    except (OSError, ValueError, KeyError):
+        return None
+    want = {"workload": args.workload, "steps": args.steps, "warmup": args.warmup, "seed": args.seed}
+    if hashlib.sha256(src).hexdigest() != rec.get("kernel_sha256") or rec.get("command_args") != want:
+        return None
+    return rec["k_gate_up"]["hbm_bytes_per_launch"]
+
+
 def moe_slab_bytes(d, f):
     import paper_2512_16473_amd as moe
     return moe.slab_bytes(d, f)
@@ -138,6 +153,8 @@ def main():
     ap.add_argument("--pinned-gb", type=float, default=56.0, help="page-locked host memory for expert copies (GiB)")
     ap.add_argument("--cpu-baseline-s", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB 5 times (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: the decode expert stage has no multi-GPU path here "
@@ -151,6 +168,15 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs the GPU"
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        nbytes = args.copy_calibration << 20
+        src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes_read": nbytes, "copy_calibration_bytes_written": nbytes}))
+        return
     wl = synth.WORKLOADS[args.workload]
     steps_total = args.warmup + args.steps
     assert steps_total <= wl.T, f"at most {wl.T} decode steps in this workload"
@@ -216,7 +242,8 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(gu_gbs / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(args),
+            "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE x2.0 + WRITE_SIZE, profiles/traffic.json)",
             "launches": st["gate_up_launches"],
             "avg_us": round(st["gate_up_ms"] / max(1, st["gate_up_launches"]) * 1e3, 2),
             "bytes_per_launch": round(st["gate_up_bytes"] / max(1, st["gate_up_launches"])),

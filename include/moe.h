@@ -204,11 +204,13 @@ void moe_runtime_destroy(moe_runtime *rt);
  *          (+ shared expert).
  * idx_host host int32 [k], w_host host fp32 [k]: routing in rank order (nullable).
  * hit_host host uint8 [k]: 1 if the expert was a cache hit (nullable).
- * compute_stream runs the router, hit FFN and combine; act_stream the hidden-state
- * and routing read-back; copy_stream the post-fetch of missed experts. The call
- * returns after the host part (miss FFN, cache update) is done and the device work
- * is enqueued. Post-fetched experts become usable from the next token at this
- * layer; that next use waits for the copy to finish.
+ * compute_stream runs the router, hit FFN and combine; copy_stream the post-fetch of
+ * missed experts. act_stream is accepted for ABI stability and may be NULL: the
+ * router kernel itself writes the routing and the hidden state into coherent pinned
+ * memory that the host polls, so activations never queue behind weight copies
+ * (Section III-C keeps them apart). The call returns after the host part (cache
+ * update, miss FFN) is done and the device work is enqueued. Post-fetched experts
+ * become usable from the next token at this layer; that next use waits for the copy.
  */
 int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out_dev,
                       int32_t *idx_host, float *w_host, uint8_t *hit_host,

@@ -84,6 +84,10 @@ SIGNATURES = [
 
 
 def load(path: str = LIB_PATH):
+    # torch ships its own HIP runtime (same soname as the system one). Loading torch
+    # first makes libmoe.so bind to that runtime, so the process has one HIP runtime
+    # and torch's streams and device memory are valid handles for the library.
+    import torch  # noqa: F401
     if not os.path.exists(path):
         raise ImportError(
             f"{path} is missing: build the HIP library first "

@@ -1,15 +1,18 @@
 // gfx950 kernels of the MoE expert stage: router gating, the hit-expert SwiGLU
-// FFN as two weight-streaming GEMV kernels, the split-K reduce + combine.
+// FFN as two weight-streaming GEMV kernels, and the fixed-order reduce + combine.
 //
 // Batch-1 decode reads every weight of a hit expert exactly once and does two
 // flops per weight, so the FFN is bound by HBM bandwidth, not by the matrix cores.
-// The kernels therefore stream each bf16 weight row with 16-byte loads per lane
-// (a 64-lane wave covers 512 contiguous weights per load), keep the activation
-// vector in registers for the whole life of the wave, reduce each row across the
-// wave with cross-lane shuffles, and spread the rows of all hit experts evenly
-// over every wave of the grid. The down projection splits its reduction (length f)
-// into segments of at most kSegMax so the activation slice a wave holds stays in
-// registers; the fixed-order sum of the segment partials is fused into the combine.
+// The kernels stream each bf16 weight row with 16-byte nontemporal loads per lane
+// (a 64-lane wave covers 512 contiguous weights per load; the weights are used once,
+// so they are not kept in the caches), keep the activation slice in registers for
+// the life of the wave, reduce each row across the wave with cross-lane shuffles,
+// and spread the rows of all hit experts evenly over every wave of the grid. The
+// down projection splits its reduction (length f) into segments of at most kSegMax
+// so the activation slice a wave holds stays in registers; each wave takes one
+// contiguous, equal share of all (segment, row) pairs, and the segment partials,
+// already scaled by the gate weight, are summed in a fixed order by the reduce.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -23,9 +26,20 @@ namespace {
 constexpr int kWave = 64;
 constexpr int kBlock = 256;
 constexpr int kWavesPerBlock = kBlock / kWave;
+constexpr int kRouterBlock = 512;
+constexpr int kMetaParts = 20;   // index in the workspace header of the partial count
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf_lo(uint32_t v) { return __uint_as_float(v << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
+
+// 16-byte load marked nontemporal (streamed weights are read exactly once).
+__device__ __forceinline__ uint4 stream_load(const uint4 *p)
+{
+    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
 
 __device__ __forceinline__ float wave_sum(float v)
 {
@@ -63,8 +77,8 @@ __device__ __forceinline__ void load8(const float *src, float *dst)
     dst[4] = v1.x; dst[5] = v1.y; dst[6] = v1.z; dst[7] = v1.w;
 }
 
-// Number of reduction segments and segment length of a down projection with
-// reduction length fj (fj a multiple of 8).
+// Reduction segments of a down projection with reduction length fj (a multiple of
+// 8), and the segment length.
 __device__ __host__ __forceinline__ int seg_count(int fj) { return (fj + kSegMax - 1) / kSegMax; }
 __device__ __host__ __forceinline__ int seg_len(int fj)
 {
@@ -72,71 +86,90 @@ __device__ __host__ __forceinline__ int seg_len(int fj)
     return (((fj + s - 1) / s) + 7) & ~7;
 }
 
-// Per-block table of the active jobs, built by the first threads of the block.
+// Per-block table of the jobs, built by the first threads of the block from the
+// selection (and the device expert->slot mirror). Inactive jobs own no work.
 struct JobLds {
-    int slot[kMaxJobs];           // slot (routed) / 0 (shared) / -1 inactive
-    int f[kMaxJobs];              // rows (gate/up) of the job, 0 if inactive
-    int start[kMaxJobs + 1];      // prefix sum of work items per job
     const uint8_t *slab[kMaxJobs];
+    float w[kMaxJobs];            // gate weight (1 for the shared expert)
+    int slot[kMaxJobs];           // slot (routed) / 0 (shared) / -1 inactive
+    int f[kMaxJobs];              // d_ffn of the job, 0 if inactive
+    int row0[kMaxJobs + 1];       // prefix of gate/up rows over jobs
+    int part0[kMaxJobs + 1];      // prefix of down segments over jobs (compact partial index)
 };
 
-// items_of(j, fj): work items of an active job for the kernel at hand.
-template <typename ItemsOf>
-__device__ __forceinline__ void build_jobs(const FfnParams &p, JobLds &t, ItemsOf items_of)
+__device__ __forceinline__ void build_jobs(const FfnParams &p, JobLds &t, bool need_w)
 {
     const int njobs = p.k + 1;
     if (threadIdx.x < njobs) {
         const int j = threadIdx.x;
         int slot = -1, fj = 0;
         const uint8_t *slab = nullptr;
+        float w = 1.0f;
         if (j < p.k) {
             const int s = p.sel[j];
             if (p.slotmap) slot = (s >= 0 && s < p.n) ? p.slotmap[s] : -1;
             else slot = s;
             if (slot >= p.nslots) slot = -1;
-            if (slot >= 0) { fj = p.f; slab = p.pool + (uint64_t)slot * p.slab_stride; }
+            if (slot >= 0) {
+                fj = p.f;
+                slab = p.pool + (uint64_t)slot * p.slab_stride;
+                if (need_w) w = p.w[j];
+            }
         } else if (p.shared && p.f_shared > 0) {
-            slot = 0; fj = p.f_shared; slab = p.shared;
+            slot = 0;
+            fj = p.f_shared;
+            slab = p.shared;
         }
         t.slot[j] = slot;
         t.f[j] = fj;
         t.slab[j] = slab;
+        t.w[j] = w;
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        int acc = 0;
+        int rows = 0, parts = 0;
         for (int j = 0; j < njobs; ++j) {
-            t.start[j] = acc;
-            if (t.slot[j] >= 0) acc += items_of(t.f[j]);
+            t.row0[j] = rows;
+            t.part0[j] = parts;
+            if (t.slot[j] >= 0) {
+                rows += t.f[j];
+                parts += seg_count(t.f[j]);
+            }
         }
-        t.start[njobs] = acc;
+        t.row0[njobs] = rows;
+        t.part0[njobs] = parts;
     }
     __syncthreads();
 }
 
-__device__ __forceinline__ int find_job(const JobLds &t, int njobs, int it)
+// Job owning item `it` of a prefix table (it < table[njobs]).
+__device__ __forceinline__ int job_of(const int *table, int njobs, int it)
 {
     int j = 0;
-    while (j + 1 < njobs && t.start[j + 1] <= it) ++j;
+    while (j + 1 < njobs && table[j + 1] <= it) ++j;
     return j;
 }
 
 // ---------------------------------------------------------------------------
 // Gate/up/SiLU: h_j[i] = SiLU(W1_j[i,:] x) * (W3_j[i,:] x) for every row i of
 // every active job. CPL = 16-byte chunks per lane along d (d <= CPL * 512).
+// Block 0 also publishes the job table and the partial count for the reduce.
 // ---------------------------------------------------------------------------
 template <int CPL>
 __global__ __launch_bounds__(kBlock) void k_gate_up(FfnParams p)
 {
     __shared__ JobLds t;
-    build_jobs(p, t, [](int fj) { return fj; });
+    build_jobs(p, t, false);
     const int njobs = p.k + 1;
-    if (blockIdx.x == 0 && threadIdx.x < njobs) p.jobslot[threadIdx.x] = t.slot[threadIdx.x];
+    if (blockIdx.x == 0) {
+        if (threadIdx.x < njobs) p.jobslot[threadIdx.x] = t.slot[threadIdx.x];
+        if (threadIdx.x == 0) p.jobslot[kMetaParts] = t.part0[njobs];
+    }
 
     const int lane = threadIdx.x & (kWave - 1);
     const int nwaves = gridDim.x * kWavesPerBlock;
     const int wid = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
-    const int total = t.start[njobs];
+    const int total = t.row0[njobs];
     if (wid >= total) return;
 
     const int d = p.d;
@@ -152,17 +185,21 @@ __global__ __launch_bounds__(kBlock) void k_gate_up(FfnParams p)
     }
 
     for (int it = wid; it < total; it += nwaves) {
-        const int j = find_job(t, njobs, it);
-        const int i = it - t.start[j];
-        const int fj = t.f[j];
+        const int j = job_of(t.row0, njobs, it);
+        const int i = it - t.row0[j];
         const uint4 *r1 = reinterpret_cast<const uint4 *>(t.slab[j] + (uint64_t)i * d * 2);
-        const uint4 *r3 = reinterpret_cast<const uint4 *>(t.slab[j] + ((uint64_t)fj * d + (uint64_t)i * d) * 2);
+        const uint4 *r3 = reinterpret_cast<const uint4 *>(t.slab[j] + ((uint64_t)t.f[j] * d + (uint64_t)i * d) * 2);
         uint4 a[CPL], b[CPL];
 #pragma unroll
         for (int c = 0; c < CPL; ++c) {
             const int ch = c * kWave + lane;
-            if (ch < nch) { a[c] = r1[ch]; b[c] = r3[ch]; }
-            else { a[c] = make_uint4(0, 0, 0, 0); b[c] = make_uint4(0, 0, 0, 0); }
+            if (ch < nch) {
+                a[c] = stream_load(r1 + ch);
+                b[c] = stream_load(r3 + ch);
+            } else {
+                a[c] = make_uint4(0, 0, 0, 0);
+                b[c] = make_uint4(0, 0, 0, 0);
+            }
         }
         float g0 = 0.f, g1 = 0.f, u0 = 0.f, u1 = 0.f;
 #pragma unroll
@@ -181,35 +218,40 @@ __global__ __launch_bounds__(kBlock) void k_gate_up(FfnParams p)
 }
 
 // ---------------------------------------------------------------------------
-// Down: partial[j][s][i] = sum over segment s of W2_j[i, c] h_j[c].
-// A work item is (job, segment, block of kRowsPerDownItem output rows); the wave
-// holds its h segment in registers and streams the rows.
+// Down: partial[part0[j] + s][i] = w_j * sum over segment s of W2_j[i, c] h_j[c].
+// The (segment, row) pairs of all active jobs, in (job, segment, row) order, are
+// split into one contiguous, equal range per wave; the wave reloads its h segment
+// (registers) only where its range crosses a segment, and streams two rows per step.
 // ---------------------------------------------------------------------------
 constexpr int kCplK = kSegMax / (8 * kWave);   // chunks per lane of one segment
 
 __global__ __launch_bounds__(kBlock) void k_down(FfnParams p)
 {
     __shared__ JobLds t;
-    const int d = p.d;
-    const int nrb = (d + kRowsPerDownItem - 1) / kRowsPerDownItem;
-    build_jobs(p, t, [nrb](int fj) { return seg_count(fj) * nrb; });
+    build_jobs(p, t, true);
     const int njobs = p.k + 1;
-
+    const int d = p.d;
     const int lane = threadIdx.x & (kWave - 1);
-    const int nwaves = gridDim.x * kWavesPerBlock;
-    const int wid = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
-    const int total = t.start[njobs];
+    const int64_t nwaves = (int64_t)gridDim.x * kWavesPerBlock;
+    const int64_t wid = (int64_t)blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    const int64_t total = (int64_t)t.part0[njobs] * d;
+    int64_t r = total * wid / nwaves;
+    const int64_t r_end = total * (wid + 1) / nwaves;
 
-    for (int it = wid; it < total; it += nwaves) {
-        const int j = find_job(t, njobs, it);
-        const int local = it - t.start[j];
-        const int s = local / nrb;
-        const int rb = local - s * nrb;
+    while (r < r_end) {
+        const int q = (int)(r / d);                 // compact segment index
+        const int j = job_of(t.part0, njobs, q);
+        const int s = q - t.part0[j];
+        const int i0 = (int)(r - (int64_t)q * d);
+        const int64_t seg_end = (int64_t)(q + 1) * d;
+        const int64_t run_end = r_end < seg_end ? r_end : seg_end;
+        const int i1 = (int)(run_end - (int64_t)q * d);
         const int fj = t.f[j];
         const int seg = seg_len(fj);
         const int c0 = s * seg;
         const int len = min(seg, fj - c0);
         const int nch = len >> 3;
+        const float wj = t.w[j];
 
         float hr[kCplK * 8];
         const float *hj = p.h + (size_t)j * p.hstride + c0;
@@ -221,21 +263,23 @@ __global__ __launch_bounds__(kBlock) void k_down(FfnParams p)
 #pragma unroll
                 for (int e = 0; e < 8; ++e) hr[c * 8 + e] = 0.f;
         }
-
         const uint8_t *w2 = t.slab[j] + (uint64_t)2 * fj * d * 2;
-        const int i0 = rb * kRowsPerDownItem;
-        const int i1 = min(d, i0 + kRowsPerDownItem);
-        float *out = p.partial + ((size_t)j * p.smax + s) * d;
+        float *out = p.partial + (size_t)q * d;
         for (int i = i0; i < i1; i += 2) {
             const bool two = (i + 1 < i1);
             const uint4 *ra = reinterpret_cast<const uint4 *>(w2 + ((uint64_t)i * fj + c0) * 2);
-            const uint4 *rb2 = reinterpret_cast<const uint4 *>(w2 + ((uint64_t)(two ? i + 1 : i) * fj + c0) * 2);
+            const uint4 *rb = reinterpret_cast<const uint4 *>(w2 + ((uint64_t)(two ? i + 1 : i) * fj + c0) * 2);
             uint4 a[kCplK], b[kCplK];
 #pragma unroll
             for (int c = 0; c < kCplK; ++c) {
                 const int ch = c * kWave + lane;
-                if (ch < nch) { a[c] = ra[ch]; b[c] = rb2[ch]; }
-                else { a[c] = make_uint4(0, 0, 0, 0); b[c] = make_uint4(0, 0, 0, 0); }
+                if (ch < nch) {
+                    a[c] = stream_load(ra + ch);
+                    b[c] = two ? stream_load(rb + ch) : make_uint4(0, 0, 0, 0);
+                } else {
+                    a[c] = make_uint4(0, 0, 0, 0);
+                    b[c] = make_uint4(0, 0, 0, 0);
+                }
             }
             float s0 = 0.f, s1 = 0.f, q0 = 0.f, q1 = 0.f;
 #pragma unroll
@@ -248,28 +292,29 @@ __global__ __launch_bounds__(kBlock) void k_down(FfnParams p)
             const float ya = wave_sum(s0 + s1);
             const float yb = wave_sum(q0 + q1);
             if (lane == 0) {
-                out[i] = ya;
-                if (two) out[i + 1] = yb;
+                out[i] = wj * ya;
+                if (two) out[i + 1] = wj * yb;
             }
         }
+        r = run_end;
     }
 }
 
-// out[i] = sum_j weight_j * sum_s partial[j][s][i] (+ y_extra[i]); fixed order.
+// out[i] = the compact partials summed in index order (+ y_extra[i]).
 __global__ __launch_bounds__(kBlock) void k_reduce(FfnParams p, const float *y_extra, float *out)
 {
     const int i = blockIdx.x * kBlock + threadIdx.x;
     if (i >= p.d) return;
+    const int nparts = p.jobslot[kMetaParts];
+    const float *src = p.partial + i;
+    const size_t ld = (size_t)p.d;
     float acc = 0.f;
-    for (int j = 0; j <= p.k; ++j) {
-        if (p.jobslot[j] < 0) continue;
-        const int fj = (j < p.k) ? p.f : p.f_shared;
-        const int S = seg_count(fj);
-        float s = 0.f;
-        for (int q = 0; q < S; ++q) s += p.partial[((size_t)j * p.smax + q) * p.d + i];
-        const float wj = (j < p.k) ? p.w[j] : 1.0f;
-        acc = fmaf(wj, s, acc);
+    int q = 0;
+    for (; q + 4 <= nparts; q += 4) {
+        const float a = src[q * ld], b = src[(q + 1) * ld], c = src[(q + 2) * ld], e = src[(q + 3) * ld];
+        acc = (((acc + a) + b) + c) + e;
     }
+    for (; q < nparts; ++q) acc += src[q * ld];
     if (y_extra) acc += y_extra[i];
     out[i] = acc;
 }
@@ -287,91 +332,170 @@ __global__ __launch_bounds__(kBlock) void k_combine(const float *a, const float 
 }
 
 // ---------------------------------------------------------------------------
-// Router: one block per token. Logits accumulate the exact fp64 products of the
-// fp32 inputs; selection and gate weights are computed in fp64 by wave 0.
-// NaN logits are ranked as -inf so the selected ids are always valid.
+// Router: one block per token. x is staged in LDS; each wave takes whole experts,
+// issuing all CPR 16-byte loads of a router row at once, and accumulates the exact
+// fp64 products of the fp32 inputs. Wave 0 then selects the top-k in fp64 (ties to
+// the lower id; NaN ranked as -inf so ids are always valid) and forms the weights.
+// CPR = float4 chunks per lane along d (d <= CPR * 256).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kBlock) void k_router(const float *X, const float *Wr, int d, int n,
-                                                   int k, int32_t *idx, float *wout)
+template <int CPR>
+__global__ __launch_bounds__(kRouterBlock) void k_router(const float *X, const float *Wr, int d, int n, int k,
+                                                         int32_t *idx, float *wout, RouteMailbox *mbox,
+                                                         float *x_host, int32_t seq)
 {
+    constexpr int kWaves = kRouterBlock / kWave;
     __shared__ double logit[MOE_MAX_EXPERTS];
+    __shared__ float4 xs[CPR * kWave];
     const int t = blockIdx.x;
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = threadIdx.x >> 6;
-    const float *x = X + (size_t)t * d;
-    for (int e = wv; e < n; e += kWavesPerBlock) {
-        const float *w = Wr + (size_t)e * d;
+    const int nq = d >> 2;   // float4 chunks of a row
+    const float4 *x4 = reinterpret_cast<const float4 *>(X + (size_t)t * d);
+    for (int q = threadIdx.x; q < CPR * kWave; q += kRouterBlock) xs[q] = q < nq ? x4[q] : make_float4(0, 0, 0, 0);
+    __syncthreads();
+    for (int e = wv; e < n; e += kWaves) {
+        const float4 *w4 = reinterpret_cast<const float4 *>(Wr + (size_t)e * d);
         double acc = 0.0;
-        for (int j = lane * 4; j < d; j += kWave * 4) {
-            const float4 xv = *reinterpret_cast<const float4 *>(x + j);
-            const float4 wvv = *reinterpret_cast<const float4 *>(w + j);
-            acc += (double)wvv.x * (double)xv.x;
-            acc += (double)wvv.y * (double)xv.y;
-            acc += (double)wvv.z * (double)xv.z;
-            acc += (double)wvv.w * (double)xv.w;
+        // Eight 16-byte loads in flight per lane per step keeps the registers bounded.
+        constexpr int kStep = CPR < 8 ? CPR : 8;
+#pragma unroll 1
+        for (int mb = 0; mb < CPR; mb += kStep) {
+            float4 wvv[kStep];
+#pragma unroll
+            for (int m = 0; m < kStep; ++m) {
+                const int q = (mb + m) * kWave + lane;
+                wvv[m] = q < nq ? w4[q] : make_float4(0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int m = 0; m < kStep; ++m) {
+                const float4 xv = xs[(mb + m) * kWave + lane];
+                acc += (double)wvv[m].x * (double)xv.x;
+                acc += (double)wvv[m].y * (double)xv.y;
+                acc += (double)wvv[m].z * (double)xv.z;
+                acc += (double)wvv[m].w * (double)xv.w;
+            }
         }
         acc = wave_sum(acc);
         if (lane == 0) logit[e] = acc;
     }
     __syncthreads();
-    if (wv != 0) return;
-
-    constexpr int kPer = MOE_MAX_EXPERTS / kWave;
-    double v[kPer];
-    bool taken[kPer];
-#pragma unroll
-    for (int q = 0; q < kPer; ++q) {
-        const int e = q * kWave + lane;
-        double l = (e < n) ? logit[e] : -INFINITY;
-        if (l != l) l = -INFINITY;
-        v[q] = l;
-        taken[q] = (e >= n);
-    }
-    // Lane r keeps the r-th selected (logit, id): order is logit desc, id asc.
-    double my_l = -INFINITY;
-    int my_i = -1;
-    for (int r = 0; r < k; ++r) {
-        double bv = -INFINITY;
-        int bi = 0x7fffffff;
+    if (wv == 0) {
+        constexpr int kPer = MOE_MAX_EXPERTS / kWave;
+        double v[kPer];
+        bool taken[kPer];
 #pragma unroll
         for (int q = 0; q < kPer; ++q) {
             const int e = q * kWave + lane;
-            if (!taken[q] && (v[q] > bv || (v[q] == bv && e < bi))) { bv = v[q]; bi = e; }
+            double l = (e < n) ? logit[e] : -INFINITY;
+            if (l != l) l = -INFINITY;
+            v[q] = l;
+            taken[q] = (e >= n);
         }
+        // Lane r keeps the r-th selected (logit, id): order is logit desc, id asc.
+        double my_l = -INFINITY;
+        int my_i = -1;
+        for (int r = 0; r < k; ++r) {
+            double bv = -INFINITY;
+            int bi = 0x7fffffff;
 #pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-            const double ov = __shfl_xor(bv, o, kWave);
-            const int oi = __shfl_xor(bi, o, kWave);
-            if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+            for (int q = 0; q < kPer; ++q) {
+                const int e = q * kWave + lane;
+                if (!taken[q] && (v[q] > bv || (v[q] == bv && e < bi))) {
+                    bv = v[q];
+                    bi = e;
+                }
+            }
+#pragma unroll
+            for (int o = 32; o > 0; o >>= 1) {
+                const double ov = __shfl_xor(bv, o, kWave);
+                const int oi = __shfl_xor(bi, o, kWave);
+                if (ov > bv || (ov == bv && oi < bi)) {
+                    bv = ov;
+                    bi = oi;
+                }
+            }
+            if (lane == r) {
+                my_l = bv;
+                my_i = bi;
+            }
+#pragma unroll
+            for (int q = 0; q < kPer; ++q)
+                if (q * kWave + lane == bi) taken[q] = true;
         }
-        if (lane == r) { my_l = bv; my_i = bi; }
-#pragma unroll
-        for (int q = 0; q < kPer; ++q)
-            if (q * kWave + lane == bi) taken[q] = true;
+        // w_r = exp(l_r - l_0) / sum_{s<k} exp(l_s - l_0), the softmax restricted to
+        // the selected set (equal to p_S / sum p_S).
+        const double l0 = __shfl(my_l, 0, kWave);
+        const double ex = (lane < k) ? exp(my_l - l0) : 0.0;
+        const double z = wave_sum(ex);
+        if (lane < k) {
+            const float wr32 = (float)(ex / z);
+            idx[(size_t)t * k + lane] = my_i;
+            wout[(size_t)t * k + lane] = wr32;
+            if (mbox) {
+                mbox->idx[lane] = my_i;
+                mbox->w[lane] = wr32;
+            }
+        }
+    } else if (x_host) {
+        // The other waves hand the hidden state to the host for the miss path.
+        float4 *xh = reinterpret_cast<float4 *>(x_host);
+        for (int q = threadIdx.x - kWave; q < nq; q += kRouterBlock - kWave) xh[q] = xs[q];
     }
-    // w_r = exp(l_r - l_0) / sum_{s<k} exp(l_s - l_0), the softmax restricted to
-    // the selected set (equal to p_S / sum p_S).
-    const double l0 = __shfl(my_l, 0, kWave);
-    const double ex = (lane < k) ? exp(my_l - l0) : 0.0;
-    const double z = wave_sum(ex);
-    if (lane < k) {
-        idx[(size_t)t * k + lane] = my_i;
-        wout[(size_t)t * k + lane] = (float)(ex / z);
+    if (mbox) {
+        __threadfence_system();
+        __syncthreads();
+        if (threadIdx.x == 0) __hip_atomic_store(&mbox->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
     }
 }
 
-template <int CPL>
-hipError_t launch_gate_up_cpl(const FfnParams &p, int blocks, hipStream_t s)
+// Resident blocks per CU of a kernel (cached by the caller). If the runtime cannot
+// answer, the count is derived from the kernel's register use (512 VGPRs per SIMD
+// lane, one wave per SIMD per 256-thread block), else 2.
+template <typename K>
+int blocks_per_cu(K kernel, int block, int *cache)
 {
-    hipLaunchKernelGGL(k_gate_up<CPL>, dim3(blocks), dim3(kBlock), 0, s, p);
+    if (*cache <= 0) {
+        int b = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, kernel, block, 0) != hipSuccess || b <= 0) {
+            (void)hipGetLastError();
+            hipFuncAttributes fa{};
+            b = 2;
+            if (hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(kernel)) == hipSuccess && fa.numRegs > 0) {
+                const int regs = (fa.numRegs + 7) & ~7;
+                b = 512 / regs;
+                if (b > 8) b = 8;
+                if (b < 1) b = 1;
+            } else {
+                (void)hipGetLastError();
+            }
+        }
+        *cache = b;
+    }
+    return *cache;
+}
+
+// Launch status: the runtime's last error is cleared before each launch (another
+// library in the process may have left one) and read right after it.
+inline void clear_launch_error() { (void)hipGetLastError(); }
+
+template <int CPL>
+hipError_t launch_gate_up_cpl(const FfnParams &p, int items, hipStream_t s, hipEvent_t e0, hipEvent_t e1)
+{
+    static int occ = 0;
+    const int cap = blocks_per_cu(k_gate_up<CPL>, kBlock, &occ) * device_cu_count() * 4;
+    int blocks = (items + kWavesPerBlock - 1) / kWavesPerBlock;
+    blocks = blocks < 1 ? 1 : (blocks > cap ? cap : blocks);
+    clear_launch_error();
+    if (e0 || e1) hipExtLaunchKernelGGL(k_gate_up<CPL>, dim3(blocks), dim3(kBlock), 0, s, e0, e1, 0, p);
+    else hipLaunchKernelGGL(k_gate_up<CPL>, dim3(blocks), dim3(kBlock), 0, s, p);
     return hipGetLastError();
 }
 
-hipError_t launch_gate_up(const FfnParams &p, int blocks, hipStream_t s)
+hipError_t launch_gate_up(const FfnParams &p, int items, hipStream_t s, hipEvent_t e0, hipEvent_t e1)
 {
     const int cpl = (p.d / 8 + kWave - 1) / kWave;
     switch (cpl) {
-#define MOE_CPL_CASE(N) case N: return launch_gate_up_cpl<N>(p, blocks, s);
+#define MOE_CPL_CASE(N) case N: return launch_gate_up_cpl<N>(p, items, s, e0, e1);
         MOE_CPL_CASE(1) MOE_CPL_CASE(2) MOE_CPL_CASE(3) MOE_CPL_CASE(4)
         MOE_CPL_CASE(5) MOE_CPL_CASE(6) MOE_CPL_CASE(7) MOE_CPL_CASE(8)
         MOE_CPL_CASE(9) MOE_CPL_CASE(10) MOE_CPL_CASE(11) MOE_CPL_CASE(12)
@@ -379,6 +503,15 @@ hipError_t launch_gate_up(const FfnParams &p, int blocks, hipStream_t s)
 #undef MOE_CPL_CASE
     default: return hipErrorInvalidValue;
     }
+}
+
+template <int CPR>
+hipError_t launch_router_cpr(const float *x, const float *wr, int T, int d, int n, int k, int32_t *idx, float *w,
+                             hipStream_t s, RouteMailbox *mbox, float *x_host, int32_t seq)
+{
+    clear_launch_error();
+    hipLaunchKernelGGL(k_router<CPR>, dim3(T), dim3(kRouterBlock), 0, s, x, wr, d, n, k, idx, w, mbox, x_host, seq);
+    return hipGetLastError();
 }
 
 }  // namespace
@@ -403,7 +536,7 @@ size_t ffn_workspace_bytes(int max_jobs, int d, int f_max)
     (void)max_jobs;
     const size_t hstride = (size_t)((f_max + 63) & ~63);
     const size_t smax = (size_t)seg_count(f_max);
-    return align256(sizeof(int32_t) * kMaxJobs) + align256(sizeof(float) * kMaxJobs * hstride) +
+    return align256(sizeof(int32_t) * 64) + align256(sizeof(float) * kMaxJobs * hstride) +
            align256(sizeof(float) * kMaxJobs * smax * (size_t)d);
 }
 
@@ -413,7 +546,7 @@ void ffn_bind_workspace(FfnParams &p, void *ws, int max_jobs, int d, int f_max)
     const size_t hstride = (size_t)((f_max + 63) & ~63);
     uint8_t *b = static_cast<uint8_t *>(ws);
     p.jobslot = reinterpret_cast<int32_t *>(b);
-    b += align256(sizeof(int32_t) * kMaxJobs);
+    b += align256(sizeof(int32_t) * 64);
     p.h = reinterpret_cast<float *>(b);
     p.hstride = (int)hstride;
     b += align256(sizeof(float) * kMaxJobs * hstride);
@@ -422,39 +555,40 @@ void ffn_bind_workspace(FfnParams &p, void *ws, int max_jobs, int d, int f_max)
 }
 
 hipError_t launch_router(const float *x, const float *wr, int T, int d, int n, int k, int32_t *idx,
-                         float *w, hipStream_t s)
+                         float *w, hipStream_t s, RouteMailbox *mbox, float *x_host, int32_t seq)
 {
     if (T <= 0) return hipSuccess;
-    hipLaunchKernelGGL(k_router, dim3(T), dim3(kBlock), 0, s, x, wr, d, n, k, idx, w);
-    return hipGetLastError();
+    if (T != 1) mbox = nullptr, x_host = nullptr;
+    const int cpr = (d / 4 + kWave - 1) / kWave;
+#define MOE_CPR_CASE(N) \
+    if (cpr <= N) return launch_router_cpr<N>(x, wr, T, d, n, k, idx, w, s, mbox, x_host, seq);
+    MOE_CPR_CASE(1) MOE_CPR_CASE(2) MOE_CPR_CASE(4) MOE_CPR_CASE(8) MOE_CPR_CASE(16) MOE_CPR_CASE(32)
+#undef MOE_CPR_CASE
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_ffn_stream(const FfnParams &p, hipStream_t s, const FfnEvents *ev, hipEvent_t after_down)
 {
-    const int cus = device_cu_count();
-    // Upper bounds of the work (every routed job active); waves with no item exit.
-    const int fmax_rows = p.k * p.f + (p.shared ? p.f_shared : 0);
-    const int nrb = (p.d + kRowsPerDownItem - 1) / kRowsPerDownItem;
-    const int down_items = p.k * seg_count(p.f) * nrb + (p.shared ? seg_count(p.f_shared) * nrb : 0);
-    auto blocks_for = [&](int items) {
-        int b = (items + kWavesPerBlock - 1) / kWavesPerBlock;
-        const int cap = cus * 8;
-        if (b > cap) b = cap;
-        return b < 1 ? 1 : b;
-    };
+    // Upper bound of the gate/up rows (every routed job active); waves with no row exit.
+    const int rows_max = p.k * p.f + (p.shared ? p.f_shared : 0);
     hipError_t e;
-    if (ev && ev->start && (e = hipEventRecord(ev->start, s)) != hipSuccess) return e;
-    if ((e = launch_gate_up(p, blocks_for(fmax_rows), s)) != hipSuccess) return e;
-    if (ev && ev->mid && (e = hipEventRecord(ev->mid, s)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_down, dim3(blocks_for(down_items)), dim3(kBlock), 0, s, p);
+    if ((e = launch_gate_up(p, rows_max, s, ev ? ev->gu_start : nullptr, ev ? ev->gu_stop : nullptr)) != hipSuccess)
+        return e;
+    static int occ_down = 0;
+    const int blocks = blocks_per_cu(k_down, kBlock, &occ_down) * device_cu_count();
+    clear_launch_error();
+    if (ev && (ev->dn_start || ev->dn_stop))
+        hipExtLaunchKernelGGL(k_down, dim3(blocks), dim3(kBlock), 0, s, ev->dn_start, ev->dn_stop, 0, p);
+    else
+        hipLaunchKernelGGL(k_down, dim3(blocks), dim3(kBlock), 0, s, p);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (ev && ev->end && (e = hipEventRecord(ev->end, s)) != hipSuccess) return e;
     if (after_down && (e = hipEventRecord(after_down, s)) != hipSuccess) return e;
     return hipSuccess;
 }
 
 hipError_t launch_ffn_reduce(const FfnParams &p, const float *y_extra, float *out, hipStream_t s)
 {
+    clear_launch_error();
     hipLaunchKernelGGL(k_reduce, dim3((p.d + kBlock - 1) / kBlock), dim3(kBlock), 0, s, p, y_extra, out);
     return hipGetLastError();
 }
@@ -462,6 +596,7 @@ hipError_t launch_ffn_reduce(const FfnParams &p, const float *y_extra, float *ou
 hipError_t launch_combine(const float *a, const float *b, const float *c, int d, float *out, hipStream_t s)
 {
     if (d <= 0) return hipSuccess;
+    clear_launch_error();
     hipLaunchKernelGGL(k_combine, dim3((d + kBlock - 1) / kBlock), dim3(kBlock), 0, s, a, b, c, d, out);
     return hipGetLastError();
 }

@@ -8,6 +8,7 @@
 namespace moe {
 
 constexpr int kMaxJobs = 17;        // up to 16 routed experts + one shared expert
+#define MOE_MAX_TOPK_INTERNAL 16
 constexpr int kSegMax = 4096;       // down-projection reduction segment (elements)
 constexpr int kRowsPerDownItem = 16;
 
@@ -39,13 +40,27 @@ struct FfnParams {
 size_t ffn_workspace_bytes(int max_jobs, int d, int f_max);
 void ffn_bind_workspace(FfnParams &p, void *ws, int max_jobs, int d, int f_max);
 
-// Events recorded around the two weight-streaming kernels (all null = no timing).
+// Events attached to the two weight-streaming kernel launches (null = no timing).
+// They are recorded by the launch itself (start and stop of that dispatch), so their
+// difference is the kernel's execution time without the dispatch gap.
 struct FfnEvents {
-    hipEvent_t start = nullptr, mid = nullptr, end = nullptr;
+    hipEvent_t gu_start = nullptr, gu_stop = nullptr, dn_start = nullptr, dn_stop = nullptr;
 };
 
+// Host-visible copy of one token's routing, written by the router kernel into
+// coherent pinned memory: the selection, the gate weights and the hidden state, then
+// `seq` (release, system scope) once everything before it is visible to the host.
+struct RouteMailbox {
+    int32_t seq;
+    int32_t pad[15];
+    int32_t idx[MOE_MAX_TOPK_INTERNAL];
+    float w[MOE_MAX_TOPK_INTERNAL];
+};
+
+// mbox/x_host (device addresses of host memory, nullable) are only used when T == 1.
 hipError_t launch_router(const float *x, const float *wr, int T, int d, int n, int k,
-                         int32_t *idx, float *w, hipStream_t s);
+                         int32_t *idx, float *w, hipStream_t s, RouteMailbox *mbox = nullptr,
+                         float *x_host = nullptr, int32_t seq = 0);
 // gate/up/SiLU then down; `after_down` (nullable) is recorded right after the down kernel.
 hipError_t launch_ffn_stream(const FfnParams &p, hipStream_t s, const FfnEvents *ev,
                              hipEvent_t after_down);

@@ -7,14 +7,20 @@
 //           off the stream that carries activations).
 //
 // Device side, in stream order on the compute stream: [wait for the previous
-// post-fetch into this layer's set] router -> gate/up/SiLU -> down -> [host miss
-// result H2D] -> reduce+combine. The hit kernels resolve expert -> slot on the
-// device from a mirror of the host slot table, so they never wait for the host.
-// The routing and the hidden state are read back on the activation stream while
-// the hit kernels run; the host then updates the LRU table, runs the misses on its
-// thread pool and enqueues the combine. Post-fetched slabs and the updated mirror
-// row land on the copy stream; the next token's use of this layer waits on that
-// copy, so the hit/miss sequence does not depend on timing.
+// post-fetch into this layer's set, if still running] router -> gate/up/SiLU ->
+// down -> reduce+combine, with no other commands between the kernels. The hit
+// kernels resolve expert -> slot on the device from a mirror of the host slot
+// table, so they never wait for the host. The router kernel itself hands the
+// routing and the hidden state to the host: it writes them into coherent pinned
+// memory followed by a sequence number, which the host polls (the activation
+// exchange never queues behind weight copies). The host then updates the LRU table,
+// starts the post-fetch copies, runs the misses on its thread pool into coherent
+// pinned memory that the reduce kernel reads directly, and enqueues the reduce.
+// The updated mirror row lands on the copy stream after this token's hit kernels;
+// the next token's use of this layer waits on that copy, so the hit/miss sequence
+// does not depend on timing.
+#include <immintrin.h>
+
 #include <chrono>
 #include <cstring>
 #include <vector>
@@ -24,12 +30,15 @@
 #include "hostpath.h"
 #include "moe_internal.h"
 
+static_assert(MOE_MAX_TOPK_INTERNAL == MOE_MAX_TOPK, "mailbox size must match the ABI bound");
+
 namespace {
 
+// Events of one timed layer call. The hit count (and so the bytes) is known on the
+// host only after the routing read-back; it is filled in then.
 struct TimingRec {
-    hipEvent_t start, mid, end;
-    int hits_gate;      // routed jobs resolved as hits are unknown on the host at
-    double bytes_gu;    // launch time; bytes are filled in from the host-side check
+    hipEvent_t ev[4];   // gate/up start, stop; down start, stop
+    double bytes_gu;
     double bytes_dn;
 };
 
@@ -47,18 +56,18 @@ struct moe_runtime {
     int32_t *d_slotmap = nullptr;   // [L][n]
     int32_t *d_idx = nullptr;       // [k]
     float *d_w = nullptr;           // [k]
-    float *d_yhost = nullptr;       // [d]
     void *d_ws = nullptr;
     size_t ws_bytes = 0;
 
-    // pinned host staging
-    int32_t *h_idx = nullptr;       // [k]
-    float *h_w = nullptr;           // [k]
-    float *h_x = nullptr;           // [d]
-    float *h_y = nullptr;           // [L][d]
+    // coherent pinned host memory shared with the kernels (host address, device address)
+    moe::RouteMailbox *mbox = nullptr, *mbox_dev = nullptr;
+    float *h_x = nullptr, *h_x_dev = nullptr;   // [d] hidden state of the current layer call
+    float *h_y = nullptr, *h_y_dev = nullptr;   // [L][d] host-path output per layer
+    int32_t seq = 0;
+    // pinned staging of the mirror rows for the copy stream
     int32_t *h_slotmap = nullptr;   // [L][n]
 
-    hipEvent_t ev_router = nullptr, ev_route = nullptr, ev_hits = nullptr;
+    hipEvent_t ev_hits = nullptr;
     std::vector<hipEvent_t> ev_fill;   // [L]
     std::vector<char> fill_pending;    // [L]
 
@@ -74,24 +83,17 @@ namespace {
 void release(moe_runtime *rt)
 {
     if (!rt) return;
-    for (auto &r : rt->pending) {
-        (void)hipEventDestroy(r.start);
-        (void)hipEventDestroy(r.mid);
-        (void)hipEventDestroy(r.end);
-    }
+    for (auto &r : rt->pending)
+        for (auto e : r.ev) (void)hipEventDestroy(e);
     for (auto e : rt->spare) (void)hipEventDestroy(e);
     for (auto e : rt->ev_fill)
         if (e) (void)hipEventDestroy(e);
-    if (rt->ev_router) (void)hipEventDestroy(rt->ev_router);
-    if (rt->ev_route) (void)hipEventDestroy(rt->ev_route);
     if (rt->ev_hits) (void)hipEventDestroy(rt->ev_hits);
     if (rt->d_slotmap) (void)hipFree(rt->d_slotmap);
     if (rt->d_idx) (void)hipFree(rt->d_idx);
     if (rt->d_w) (void)hipFree(rt->d_w);
-    if (rt->d_yhost) (void)hipFree(rt->d_yhost);
     if (rt->d_ws) (void)hipFree(rt->d_ws);
-    if (rt->h_idx) (void)hipHostFree(rt->h_idx);
-    if (rt->h_w) (void)hipHostFree(rt->h_w);
+    if (rt->mbox) (void)hipHostFree(rt->mbox);
     if (rt->h_x) (void)hipHostFree(rt->h_x);
     if (rt->h_y) (void)hipHostFree(rt->h_y);
     if (rt->h_slotmap) (void)hipHostFree(rt->h_slotmap);
@@ -115,18 +117,16 @@ int resolve_timing(moe_runtime *rt)
 {
     for (auto &r : rt->pending) {
         float a = 0.f, b = 0.f;
-        MOE_HIP(hipEventSynchronize(r.end));
-        MOE_HIP(hipEventElapsedTime(&a, r.start, r.mid));
-        MOE_HIP(hipEventElapsedTime(&b, r.mid, r.end));
+        MOE_HIP(hipEventSynchronize(r.ev[3]));
+        MOE_HIP(hipEventElapsedTime(&a, r.ev[0], r.ev[1]));
+        MOE_HIP(hipEventElapsedTime(&b, r.ev[2], r.ev[3]));
         rt->stats.gate_up_launches += 1;
         rt->stats.gate_up_ms += a;
         rt->stats.gate_up_bytes += r.bytes_gu;
         rt->stats.down_launches += 1;
         rt->stats.down_ms += b;
         rt->stats.down_bytes += r.bytes_dn;
-        rt->spare.push_back(r.start);
-        rt->spare.push_back(r.mid);
-        rt->spare.push_back(r.end);
+        for (auto e : r.ev) rt->spare.push_back(e);
     }
     rt->pending.clear();
     return MOE_OK;
@@ -190,12 +190,20 @@ int moe_runtime_create(const moe_layer_desc *desc, moe_runtime **out)
     if ((e = hipMalloc((void **)&rt->d_slotmap, sizeof(int32_t) * nh)) != hipSuccess) return fail(e, "hipMalloc");
     if ((e = hipMalloc((void **)&rt->d_idx, sizeof(int32_t) * D.k)) != hipSuccess) return fail(e, "hipMalloc");
     if ((e = hipMalloc((void **)&rt->d_w, sizeof(float) * D.k)) != hipSuccess) return fail(e, "hipMalloc");
-    if ((e = hipMalloc((void **)&rt->d_yhost, sizeof(float) * D.d)) != hipSuccess) return fail(e, "hipMalloc");
-    if ((e = hipHostMalloc((void **)&rt->h_idx, sizeof(int32_t) * D.k, 0)) != hipSuccess) return fail(e, "hipHostMalloc");
-    if ((e = hipHostMalloc((void **)&rt->h_w, sizeof(float) * D.k, 0)) != hipSuccess) return fail(e, "hipHostMalloc");
-    if ((e = hipHostMalloc((void **)&rt->h_x, sizeof(float) * D.d, 0)) != hipSuccess) return fail(e, "hipHostMalloc");
-    if ((e = hipHostMalloc((void **)&rt->h_y, sizeof(float) * D.d * (size_t)D.n_layers, 0)) != hipSuccess)
-        return fail(e, "hipHostMalloc");
+    const unsigned coherent = hipHostMallocCoherent | hipHostMallocMapped;
+    if ((e = hipHostMalloc((void **)&rt->mbox, sizeof(moe::RouteMailbox), coherent)) != hipSuccess)
+        return fail(e, "hipHostMalloc(mailbox)");
+    if ((e = hipHostMalloc((void **)&rt->h_x, sizeof(float) * D.d, coherent)) != hipSuccess)
+        return fail(e, "hipHostMalloc(x)");
+    if ((e = hipHostMalloc((void **)&rt->h_y, sizeof(float) * D.d * (size_t)D.n_layers, coherent)) != hipSuccess)
+        return fail(e, "hipHostMalloc(y)");
+    std::memset(rt->mbox, 0, sizeof(moe::RouteMailbox));
+    if ((e = hipHostGetDevicePointer((void **)&rt->mbox_dev, rt->mbox, 0)) != hipSuccess)
+        return fail(e, "hipHostGetDevicePointer");
+    if ((e = hipHostGetDevicePointer((void **)&rt->h_x_dev, rt->h_x, 0)) != hipSuccess)
+        return fail(e, "hipHostGetDevicePointer");
+    if ((e = hipHostGetDevicePointer((void **)&rt->h_y_dev, rt->h_y, 0)) != hipSuccess)
+        return fail(e, "hipHostGetDevicePointer");
     if ((e = hipHostMalloc((void **)&rt->h_slotmap, sizeof(int32_t) * nh, 0)) != hipSuccess)
         return fail(e, "hipHostMalloc");
     // Mirror of the host table as it stands now.
@@ -203,8 +211,6 @@ int moe_runtime_create(const moe_layer_desc *desc, moe_runtime **out)
         std::memcpy(rt->h_slotmap + (size_t)l * D.n, &c->where[(size_t)l * D.n], sizeof(int32_t) * D.n);
     if ((e = hipMemcpy(rt->d_slotmap, rt->h_slotmap, sizeof(int32_t) * nh, hipMemcpyHostToDevice)) != hipSuccess)
         return fail(e, "hipMemcpy(slotmap)");
-    if ((e = hipEventCreateWithFlags(&rt->ev_router, hipEventDisableTiming)) != hipSuccess) return fail(e, "event");
-    if ((e = hipEventCreateWithFlags(&rt->ev_route, hipEventDisableTiming)) != hipSuccess) return fail(e, "event");
     if ((e = hipEventCreateWithFlags(&rt->ev_hits, hipEventDisableTiming)) != hipSuccess) return fail(e, "event");
     rt->ev_fill.assign(D.n_layers, nullptr);
     rt->fill_pending.assign(D.n_layers, 0);
@@ -231,23 +237,27 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
     const moe_layer_desc &D = rt->desc;
     MOE_REQUIRE(layer >= 0 && layer < D.n_layers, "moe_layer_forward: layer=%d out of [0,%d)", layer, D.n_layers);
     MOE_REQUIRE(moe::aligned16(x_dev) && moe::aligned16(out_dev), "moe_layer_forward: x/out not 16-byte aligned");
-    hipStream_t sc = (hipStream_t)compute_stream, sa = (hipStream_t)act_stream, sw = (hipStream_t)copy_stream;
+    (void)act_stream;   // the router kernel hands routing and x to the host directly
+    hipStream_t sc = (hipStream_t)compute_stream, sw = (hipStream_t)copy_stream;
     const int d = D.d, n = D.n, k = D.k;
 
     // The previous post-fetch into this set (slabs and mirror row) must be complete
-    // before this token routes through the layer.
-    if (rt->fill_pending[layer]) MOE_HIP(hipStreamWaitEvent(sc, rt->ev_fill[layer], 0));
+    // before this token routes through the layer; skip the wait once it is.
+    if (rt->fill_pending[layer]) {
+        const hipError_t q = hipEventQuery(rt->ev_fill[layer]);
+        if (q == hipSuccess) {
+            rt->fill_pending[layer] = 0;
+        } else {
+            if (q != hipErrorNotReady) MOE_HIP(q);
+            (void)hipGetLastError();
+            MOE_HIP(hipStreamWaitEvent(sc, rt->ev_fill[layer], 0));
+        }
+    }
 
-    // Router on the compute stream; read-back of routing and hidden state on the
-    // activation stream.
+    // Router; it publishes the routing and x to the host through the mailbox.
+    const int32_t seq = ++rt->seq;
     const float *wr = D.w_router + (size_t)layer * n * d;
-    MOE_HIP(moe::launch_router(x_dev, wr, 1, d, n, k, rt->d_idx, rt->d_w, sc));
-    MOE_HIP(hipEventRecord(rt->ev_router, sc));
-    MOE_HIP(hipStreamWaitEvent(sa, rt->ev_router, 0));
-    MOE_HIP(hipMemcpyAsync(rt->h_idx, rt->d_idx, sizeof(int32_t) * k, hipMemcpyDeviceToHost, sa));
-    MOE_HIP(hipMemcpyAsync(rt->h_w, rt->d_w, sizeof(float) * k, hipMemcpyDeviceToHost, sa));
-    MOE_HIP(hipMemcpyAsync(rt->h_x, x_dev, sizeof(float) * d, hipMemcpyDeviceToHost, sa));
-    MOE_HIP(hipEventRecord(rt->ev_route, sa));
+    MOE_HIP(moe::launch_router(x_dev, wr, 1, d, n, k, rt->d_idx, rt->d_w, sc, rt->mbox_dev, rt->h_x_dev, seq));
 
     // Hit experts on the device (slots from the device mirror of the table).
     moe::FfnParams p{};
@@ -268,26 +278,33 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
     moe::FfnEvents ev;
     TimingRec rec{};
     if (rt->timing) {
-        rec.start = take_event(rt);
-        rec.mid = take_event(rt);
-        rec.end = take_event(rt);
-        MOE_REQUIRE(rec.start && rec.mid && rec.end, "moe_layer_forward: could not create timing events");
-        ev.start = rec.start;
-        ev.mid = rec.mid;
-        ev.end = rec.end;
+        for (auto &e : rec.ev) {
+            e = take_event(rt);
+            MOE_REQUIRE(e, "moe_layer_forward: could not create timing events");
+        }
+        ev.gu_start = rec.ev[0];
+        ev.gu_stop = rec.ev[1];
+        ev.dn_start = rec.ev[2];
+        ev.dn_stop = rec.ev[3];
     }
-    MOE_HIP(moe::launch_ffn_stream(p, sc, rt->timing ? &ev : nullptr, rt->ev_hits));
+    MOE_HIP(moe::launch_ffn_stream(p, sc, rt->timing ? &ev : nullptr, nullptr));
 
-    // Step 1 on the host: the routing read-back, then check + LRU update.
+    // Step 1 on the host: wait for the routing, then check + LRU update.
     const double t0 = now_ms();
-    MOE_HIP(hipEventSynchronize(rt->ev_route));
-    const double t1 = now_ms();
-    rt->stats.route_wait_ms += t1 - t0;
+    for (uint64_t spins = 0;; ++spins) {
+        if (__atomic_load_n(&rt->mbox->seq, __ATOMIC_ACQUIRE) == seq) break;
+        if ((spins & 0xffff) == 0xffff && now_ms() - t0 > 60000.0) {
+            moe::set_error("moe_layer_forward: routing of layer %d not published within 60 s", layer);
+            return MOE_EHIP;
+        }
+        _mm_pause();
+    }
+    rt->stats.route_wait_ms += now_ms() - t0;
     int32_t sel[MOE_MAX_TOPK], fill[MOE_MAX_TOPK], evicted[MOE_MAX_TOPK];
     float wsel[MOE_MAX_TOPK];
     uint8_t hit[MOE_MAX_TOPK];
-    std::memcpy(sel, rt->h_idx, sizeof(int32_t) * k);
-    std::memcpy(wsel, rt->h_w, sizeof(float) * k);
+    std::memcpy(sel, rt->mbox->idx, sizeof(int32_t) * k);
+    std::memcpy(wsel, rt->mbox->w, sizeof(float) * k);
     MOE_REQUIRE(rt->cache->valid_selection(sel, k), "moe_layer_forward: router returned an invalid selection");
     rt->cache->check(layer, sel, k, nullptr, hit);
     rt->cache->step(layer, sel, k, fill, evicted);
@@ -296,7 +313,10 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
     const void *mslab[MOE_MAX_TOPK];
     float mw[MOE_MAX_TOPK];
     for (int j = 0; j < k; ++j) {
-        if (hit[j]) { ++nhit; continue; }
+        if (hit[j]) {
+            ++nhit;
+            continue;
+        }
         mslab[nmiss] = rt->host_slabs[(size_t)layer * n + sel[j]];
         mw[nmiss] = wsel[j];
         ++nmiss;
@@ -308,20 +328,9 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
         rt->pending.push_back(rec);
     }
 
-    // Step 2(b): misses on the host thread pool, result copied in for the combine.
-    float *yh = rt->h_y + (size_t)layer * d;
-    if (nmiss) {
-        const double t2 = now_ms();
-        rt->pool->expert_ffn(rt->h_x, mslab, mw, nmiss, d, D.f, yh);
-        rt->stats.host_ffn_ms += now_ms() - t2;
-        MOE_HIP(hipMemcpyAsync(rt->d_yhost, yh, sizeof(float) * d, hipMemcpyHostToDevice, sc));
-    }
-    MOE_HIP(moe::launch_ffn_reduce(p, nmiss ? rt->d_yhost : nullptr, out_dev, sc));
-
-    // Step 3: post-fetch of the missed experts into their victim slots. The slabs
-    // can land at once (no current-token expert is ever a victim and the previous
-    // token's kernels on this layer finished before this token's router); the mirror
-    // row is rewritten only after this token's hit kernels have read it.
+    // Step 3 starts first: post-fetch of the missed experts into their victim slots.
+    // The slabs can land at once: no current-token expert is ever a victim, and the
+    // previous token's kernels on this layer finished before this token's router.
     if (nmiss) {
         uint8_t *set_base = static_cast<uint8_t *>(D.slot_pool) + (size_t)layer * D.ways * rt->slab_bytes;
         for (int j = 0; j < k; ++j) {
@@ -331,8 +340,22 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
                                    hipMemcpyHostToDevice, sw));
             rt->stats.fills += 1;
         }
+    }
+
+    // Step 2(b): misses on the host thread pool, written where the reduce reads them.
+    if (nmiss) {
+        float *yh = rt->h_y + (size_t)layer * d;
+        const double t2 = now_ms();
+        rt->pool->expert_ffn(rt->h_x, mslab, mw, nmiss, d, D.f, yh);
+        rt->stats.host_ffn_ms += now_ms() - t2;
+    }
+    MOE_HIP(moe::launch_ffn_reduce(p, nmiss ? rt->h_y_dev + (size_t)layer * d : nullptr, out_dev, sc));
+
+    // The mirror row is rewritten after this token's hit kernels have read it.
+    if (nmiss) {
         int32_t *row = rt->h_slotmap + (size_t)layer * n;
         std::memcpy(row, &rt->cache->where[(size_t)layer * n], sizeof(int32_t) * n);
+        MOE_HIP(hipEventRecord(rt->ev_hits, sc));
         MOE_HIP(hipStreamWaitEvent(sw, rt->ev_hits, 0));
         MOE_HIP(hipMemcpyAsync(rt->d_slotmap + (size_t)layer * n, row, sizeof(int32_t) * n, hipMemcpyHostToDevice, sw));
         MOE_HIP(hipEventRecord(rt->ev_fill[layer], sw));
