@@ -137,6 +137,68 @@ def measured_traffic(args):
     return rec["k_gate_up"]["hbm_bytes_per_launch"]
 
 
+def bench_prefill(args, torch, moe, synth, wl):
+    """One prompt of wl.T tokens through every layer, all experts resident in HBM
+    (L x n slabs, layers visited in order so no slab is reused while cached)."""
+    import numpy as np
+    d, f, n, k, L, T = wl.d, wl.f, wl.n, wl.k, wl.L, wl.T
+    stride = moe.slab_bytes(d, f)
+    t0 = time.perf_counter()
+    pool = torch.empty(L * n * stride, dtype=torch.uint8, device="cuda")
+    for l in range(L):
+        for e in range(n):
+            off = (l * n + e) * stride
+            t = pool[off: off + 3 * d * f * 2].view(torch.bfloat16)
+            synth.expert_slab_torch(synth.seed_for(args.seed, wl.name, "expert", l, e), d, f, wl.w_std, out=t)
+    wr = torch.stack([synth.router_weights_torch(synth.seed_for(args.seed, wl.name, "router", l), n, d)
+                      for l in range(L)]).contiguous()
+    X = torch.from_numpy(synth.iid_states(synth.seed_for(args.seed, wl.name, "prompt"), T, d)).cuda()
+    out = torch.empty((T, d), device="cuda")
+    ws = torch.empty(moe.prefill_workspace_bytes(d, f, n, k, T), dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    log(f"prefill world ready in {time.perf_counter() - t0:.1f}s ({pool.numel() / 1e9:.1f} GB of experts in HBM)")
+
+    def step():
+        for l in range(L):
+            moe.prefill_forward(X, wr[l], pool[l * n * stride:(l + 1) * n * stride], d, f, n, k, out, ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t1 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t1
+    ms = e0.elapsed_time(e1)
+    per_layer_us = ms * 1e3 / (args.steps * L)
+    bytes_layer = n * 3 * d * f * 2.0
+    flops_layer = 2.0 * 3 * d * f * T * k
+    hbm = bytes_layer / (per_layer_us * 1e-6) / 1e9
+    tf = flops_layer / (per_layer_us * 1e-6) / 1e12
+    return {
+        "metric": "prefill MoE-layer tokens/s + achieved HBM GB/s (%peak), Mixtral-8x7B shape",
+        "value": round(T * args.steps / wall, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.desc, "d_model": d, "d_ffn": f, "experts": n, "top_k": k, "layers": L,
+                   "prompt_tokens": T, "weights": "bf16, activations rounded to bf16, fp32 accumulate",
+                   "parallelism": "single GPU"},
+        "roofline": {"kernel": "prefill layer (router, grouping, grouped MFMA GEMMs, combine)", "bound": "hbm",
+                     "achieved": round(hbm, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(hbm / HBM_PEAK_GBS, 4), "traffic": None,
+                     "mfma_tflops": round(tf, 1), "mfma_peak_tflops": 2500.0, "mfma_frac": round(tf / 2500.0, 4),
+                     "us_per_layer": round(per_layer_us, 2)},
+        "cpu_baseline": None,
+    }
+
+
 def moe_slab_bytes(d, f):
     import paper_2512_16473_amd as moe
     return moe.slab_bytes(d, f)
@@ -147,7 +209,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=32)
     ap.add_argument("--warmup", type=int, default=8)
-    ap.add_argument("--workload", default="mixtral", choices=["mixtral", "phi", "fine", "tiny"])
+    ap.add_argument("--workload", default="mixtral", choices=["mixtral", "phi", "fine", "tiny", "prefill"])
     ap.add_argument("--threads", type=int, default=0, help="host expert threads (0: OMP_NUM_THREADS or all cores)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--pinned-gb", type=float, default=56.0, help="page-locked host memory for expert copies (GiB)")
@@ -178,6 +240,9 @@ def main():
         print(json.dumps({"copy_calibration_bytes_read": nbytes, "copy_calibration_bytes_written": nbytes}))
         return
     wl = synth.WORKLOADS[args.workload]
+    if wl.prefill:
+        print(json.dumps(bench_prefill(args, torch, moe, synth, wl)), flush=True)
+        return
     steps_total = args.warmup + args.steps
     assert steps_total <= wl.T, f"at most {wl.T} decode steps in this workload"
     world = build_world(torch, moe, synth, wl, steps_total, args.seed, args.threads, args.pinned_gb)

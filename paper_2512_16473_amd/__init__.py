@@ -275,6 +275,7 @@ def prefill_workspace_bytes(d, f, n, k, T) -> int:
 
 
 def prefill_forward(X, w_router, expert_pool, d, f, n, k, OUT, workspace, idx=None, w=None, stream=None):
+    """OUT[t] = routed SwiGLU expert output of X[t] (all experts resident in expert_pool)."""
     T = X.shape[0]
     P = PrefillDesc(d, f, n, k, w_router.data_ptr(), expert_pool.data_ptr())
     _check("moe_prefill_forward", _lib.moe_prefill_forward(
