@@ -122,6 +122,30 @@ def cpu_baseline(wl, world, seed, budget_s, t_first):
     }
 
 
+def host_sweep(moe, wl, world, threads_list=(1, 2, 4, 8, 16)):
+    """Host expert path alone: one layer's k experts all missed (the CPU column of the
+    paper's Table III), for several thread counts, nothing else running."""
+    import numpy as np
+    d, f, k = wl.d, wl.f, wl.k
+    stride = world["stride"]
+    host = world["hosts"][0]
+    slabs = [host.array[e * stride: e * stride + 3 * d * f * 2] for e in range(k)]
+    x = world["X"][0, 0]
+    w = np.full(k, 1.0 / k, np.float32)
+    out = {}
+    for t in threads_list:
+        pool = moe.HostPool(t)
+        times = []
+        for _ in range(3):
+            t0 = time.perf_counter()
+            pool.expert_ffn(x, slabs, w, d, f)
+            times.append(time.perf_counter() - t0)
+        pool.close()
+        ms = sorted(times)[1] * 1e3
+        out[str(t)] = {"ms": round(ms, 2), "GB/s": round(k * 3 * d * f * 2 / (ms * 1e-3) / 1e9, 1)}
+    return out
+
+
 def measured_traffic(args):
     """HBM bytes per k_gate_up launch from the committed PMC record, if it was taken on
     the current kernel source and the same workload arguments; else None."""
@@ -329,6 +353,10 @@ def main():
         },
     }
     log(json.dumps(result["trace"]), json.dumps(result["hit_ffn"]))
+    result["host_expert_layer"] = {
+        "what": f"host FFN of one layer's {k} experts (all missed), alone, by thread count",
+        "by_threads": host_sweep(moe, wl, world)}
+    log(json.dumps(result["host_expert_layer"]))
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, world, args.seed, args.cpu_baseline_s, args.warmup)
     else:
