@@ -6,16 +6,17 @@
 //      giving per-expert offsets, the sorted pair list and its inverse;
 //   3. hidden states rounded to bf16 for the matrix cores;
 //   4. grouped GEMM gate/up: for each expert e, H_e = SiLU(X_e W1_e^T) * (X_e W3_e^T),
-//      bf16 MFMA (v_mfma_f32_32x32x16_bf16) with fp32 accumulation, H_e stored bf16;
-//   5. grouped GEMM down: Y_e = H_e W2_e^T, split in two along f, fp32 partials;
+//      bf16 MFMA (v_mfma_f32_16x16x32_bf16) with fp32 accumulation, H_e stored bf16;
+//   5. grouped GEMM down: Y_e = H_e W2_e^T, K split in four (or two), fp32 partials;
 //   6. combine: OUT[t] = sum_r w[t][r] * Y[pair(t, r)], in a fixed order.
 //
-// Both GEMM operands are K-contiguous rows (token rows of X or H, weight rows of W), so
-// every lane's MFMA operand is one 16-byte run of a row. Tiles are staged through LDS
-// with a register prefetch of the next K step. Work items (expert, M tile, N tile,
-// K split) are laid out so that every item of one expert lands on the same XCD (work
-// group b runs on XCD b mod 8) and the M tiles sharing a weight tile run back to back,
-// so a weight tile is fetched from HBM once and re-read from that XCD's L2.
+// With about T k / n tokens per expert (128 for a 512-token prompt on 8 experts, top-2)
+// the GEMMs are bound by reading the expert weights from HBM, so the kernel is built to
+// keep many weight bytes in flight: the weight operand goes straight from HBM into MFMA
+// registers, several K steps ahead, and only the token tile is staged through LDS.
+// Work items (expert, M tile, N tile, K split) are laid out so that every item of one
+// expert lands on the same XCD (work group b runs on XCD b mod 8), where its token rows
+// stay in that XCD's L2.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -32,12 +33,10 @@ typedef float floatx16_t __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kThreads = 256;
-constexpr int kBM = 128;        // tokens per tile
 constexpr int kBK = 64;         // K per stage
-constexpr int kBRows = 128;     // weight rows per tile (gate/up: 64 of W1 + 64 of W3)
 constexpr int kLdsStride = kBK + 8;   // bf16 per LDS row (16-byte pad against bank conflicts)
 constexpr int kXcds = 8;
-constexpr int kDownSplits = 2;
+constexpr int kMaxDownSplits = 4;
 
 __device__ __forceinline__ uint16_t f2bf(float f)
 {
@@ -63,49 +62,56 @@ __global__ __launch_bounds__(kThreads) void k_cast_bf16(const float *x, uint16_t
 
 // Stable counting sort of the pairs p = t*k + r by expert idx[p] (one block).
 // off[e] .. off[e+1] is expert e's range in `perm` (pair ids in increasing order);
-// pos[p] is the place of pair p in that order.
-constexpr int kGroupChunk = 8192;
-__global__ __launch_bounds__(kThreads) void k_group(const int32_t *idx, int npairs, int n, int32_t *off,
-                                                    int32_t *perm, int32_t *pos)
+// pos[p] is the place of pair p in that order. The per-expert counts come from LDS
+// atomics; the place of a pair within its expert is the number of earlier pairs with
+// the same expert, counted over the chunk's ids in LDS four at a time.
+constexpr int kGroupThreads = 1024;
+__global__ __launch_bounds__(kGroupThreads) void k_group(const int32_t *idx, int npairs, int n, int32_t *off,
+                                                         int32_t *perm, int32_t *pos)
 {
-    __shared__ uint8_t ids[kGroupChunk];
-    __shared__ int32_t cnt[kThreads + 1];
-    const int e = threadIdx.x;
-    int c = 0;
-    for (int base = 0; base < npairs; base += kGroupChunk) {
-        const int m = min(kGroupChunk, npairs - base);
-        __syncthreads();
-        for (int i = threadIdx.x; i < m; i += kThreads) ids[i] = (uint8_t)idx[base + i];
-        __syncthreads();
-        if (e < n)
-            for (int i = 0; i < m; ++i) c += (ids[i] == e);
-    }
-    cnt[e] = c;
+    __shared__ int32_t base[MOE_MAX_EXPERTS];    // counts, then the next free place of each expert
+    __shared__ int32_t hist[MOE_MAX_EXPERTS];
+    __shared__ uint32_t ids32[kGroupThreads / 4];
+    uint8_t *ids = reinterpret_cast<uint8_t *>(ids32);
+    const int t = threadIdx.x;
+    for (int e = t; e < n; e += kGroupThreads) base[e] = 0;
     __syncthreads();
-    if (threadIdx.x == 0) {
+    for (int p = t; p < npairs; p += kGroupThreads) atomicAdd(&base[idx[p]], 1);
+    __syncthreads();
+    if (t == 0) {
         int acc = 0;
-        for (int q = 0; q < n; ++q) {
-            const int v = cnt[q];
-            cnt[q] = acc;
-            off[q] = acc;
-            acc += v;
+        for (int e = 0; e < n; ++e) {
+            const int c = base[e];
+            base[e] = acc;
+            off[e] = acc;
+            acc += c;
         }
         off[n] = acc;
     }
-    __syncthreads();
-    int w = cnt[e];
-    for (int base = 0; base < npairs; base += kGroupChunk) {
-        const int m = min(kGroupChunk, npairs - base);
+    for (int c0 = 0; c0 < npairs; c0 += kGroupThreads) {
+        const int m = min(kGroupThreads, npairs - c0);
+        const int my = t < m ? idx[c0 + t] : 0;
         __syncthreads();
-        for (int i = threadIdx.x; i < m; i += kThreads) ids[i] = (uint8_t)idx[base + i];
+        if (t < m) ids[t] = (uint8_t)my;
+        for (int e = t; e < n; e += kGroupThreads) hist[e] = 0;
         __syncthreads();
-        if (e < n)
-            for (int i = 0; i < m; ++i)
-                if (ids[i] == e) {
-                    perm[w] = base + i;
-                    pos[base + i] = w;
-                    ++w;
-                }
+        if (t < m) {
+            // rank = number of j < t with ids[j] == my (a zero byte of ids ^ my marks a match)
+            const uint32_t pat = 0x01010101u * (uint32_t)my;
+            int rank = 0;
+            for (int j = 0; j < (t >> 2); ++j) {
+                const uint32_t x = ids32[j] ^ pat;
+                const uint32_t z = ~(((x & 0x7F7F7F7Fu) + 0x7F7F7F7Fu) | x | 0x7F7F7F7Fu);
+                rank += __popc(z);
+            }
+            for (int j = t & ~3; j < t; ++j) rank += ids[j] == (uint8_t)my;
+            const int w = base[my] + rank;
+            perm[w] = c0 + t;
+            pos[c0 + t] = w;
+            atomicAdd(&hist[my], 1);
+        }
+        __syncthreads();
+        for (int e = t; e < n; e += kGroupThreads) base[e] += hist[e];
     }
 }
 
@@ -124,15 +130,40 @@ struct GemmArgs {
     float *yp;                // down output, fp32 [ksplit][P][d]
 };
 
-// Grouped GEMM, one 128 x 128 output tile per work group (gate/up: 128 tokens x
-// (64 gate + 64 up) rows; down: 128 tokens x 128 output rows), 4 waves as 2 x 2.
-template <bool kGateUp>
-__global__ __launch_bounds__(kThreads) void k_group_gemm(GemmArgs g)
-{
-    __shared__ uint16_t lds_a[2][kBM * kLdsStride];
-    __shared__ uint16_t lds_b[2][kBRows * kLdsStride];
+// Grouped GEMM with the weight operand fed straight from HBM into MFMA registers.
+//
+// A work group (8 waves) owns up to 192 tokens of one expert and 128 kNB weight rows; each
+// wave owns 16 kNB of the weight rows (kNB 16-row MFMA column blocks) and all the tokens
+// (twelve 16-row blocks). In v_mfma_f32_16x16x32_bf16 the B operand of lane l is 8
+// consecutive K values of column l mod 16, the four lanes l mod 16 + 16 i covering 32
+// consecutive K values, so each lane loads its 16-byte B pieces from its own weight
+// row: weights never pass through LDS, each weight byte is loaded once per work group,
+// and every load instruction reads 64 contiguous bytes from each of 16 rows (with the
+// 32x32x16 shape it would be 32 bytes from 32 rows, which halves the rate HBM delivers).
+// Only the token tile (shared by the 8 waves) is staged in LDS, double-buffered.
+// Loads run kS K steps ahead in a ring of kS register sets; the K loop is unrolled by kS
+// so that every set is a fixed group of registers and each wait covers exactly the
+// oldest set. All loads are unconditional: token rows past the tile re-read row 0 (their
+// outputs are dropped) and steps past the end re-read the last step.
+//
+// gate/up: a wave's two column blocks are 16 W1 rows and the same 16 W3 rows, so the gate
+// and up values of an output sit in the same lane. down: kNB blocks of 16 consecutive W2
+// rows (kNB = 1 when d is not a multiple of 256); K = f is split in ksplit parts that write
+// separate fp32 partial sums.
+typedef float floatx4_t __attribute__((ext_vector_type(4)));
+constexpr int kGThreads = 512;
+constexpr int kGWaves = kGThreads / 64;
+constexpr int kMBlocks = 12;                           // 16-token blocks per tile
+constexpr int kTileM = kMBlocks * 16;                  // 192 tokens
+constexpr int kANum = kTileM * 8 / kGThreads;          // token-tile 16-byte chunks per thread per step
+constexpr int kKBlocks = kBK / 32;                     // MFMA K blocks per step
+static_assert(kTileM * 8 % kGThreads == 0, "token tile must split evenly over the threads");
 
-    // work item -> (expert, m tile, n tile, k split); all items of an expert on one XCD
+template <bool kGateUp, int kS, int kNB>
+__global__ __launch_bounds__(kGThreads) void k_moe_gemm(GemmArgs g)
+{
+    __shared__ uint16_t lds_a[2][kTileM * kLdsStride];
+
     const int xcd = blockIdx.x % kXcds;
     int q = blockIdx.x / kXcds;
     if (q >= g.per_xcd) return;
@@ -144,149 +175,150 @@ __global__ __launch_bounds__(kThreads) void k_group_gemm(GemmArgs g)
     q /= g.ksplit;
     const int mt = q % g.mtiles;
     const int nt = q / g.mtiles;
-    const int row0 = g.off[e] + mt * kBM;          // first pair row of this tile
-    const int rows = min(kBM, g.off[e + 1] - row0);
+    const int row0 = g.off[e] + mt * kTileM;
+    const int rows = min(kTileM, g.off[e + 1] - row0);
     if (rows <= 0) return;
 
     const int K = kGateUp ? g.d : g.f;
     const int kspan = K / g.ksplit;
     const int k0 = ks * kspan;
     const int nsteps = kspan / kBK;
-    const uint8_t *slab = g.pool + (uint64_t)e * g.slab_stride;
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const uint16_t *w = reinterpret_cast<const uint16_t *>(g.pool + (uint64_t)e * g.slab_stride);
 
-    // Global sources of the 4 A chunks and 4 B chunks this thread stages per step
-    // (chunk c = tid + 256 i: row c / 8, 16-byte column c % 8).
-    const uint16_t *asrc[4];
-    const uint16_t *bsrc[4];
-    bool avalid[4];
+    static_assert(!kGateUp || kNB == 2, "gate/up pairs a W1 block with a W3 block");
+    // this lane's weight rows (MFMA column lane mod 16 of each column block) and K offset
+    const uint16_t *bsrc[kNB];
+    if (kGateUp) {
+        const size_t wrow = (size_t)nt * 128 + wv * 16 + (lane & 15);
+        bsrc[0] = w + wrow * g.d + k0 + 8 * (lane >> 4);
+        bsrc[1] = w + (size_t)g.f * g.d + wrow * g.d + k0 + 8 * (lane >> 4);
+    } else {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int c = tid + kThreads * i;
+        for (int nb = 0; nb < kNB; ++nb) {
+            const size_t wrow = (size_t)nt * (kGWaves * 16 * kNB) + wv * 16 * kNB + nb * 16 + (lane & 15);
+            bsrc[nb] = w + (size_t)2 * g.f * g.d + wrow * g.f + k0 + 8 * (lane >> 4);
+        }
+    }
+    // token-tile chunks staged by this thread: chunk c = tid + 512 i is row c / 8, 16-byte column c % 8
+    const uint16_t *asrc[kANum];
+#pragma unroll
+    for (int i = 0; i < kANum; ++i) {
+        const int c = tid + kGThreads * i;
         const int r = c >> 3, col = (c & 7) * 8;
-        avalid[i] = r < rows;
-        const int rr = avalid[i] ? r : 0;
-        if (kGateUp) {
-            const int token = g.perm[row0 + rr] / g.k;
-            asrc[i] = g.a + (size_t)token * g.d + k0 + col;
-            const uint16_t *w = reinterpret_cast<const uint16_t *>(slab);
-            const int wrow = nt * 64 + (r & 63);
-            bsrc[i] = (r < 64) ? w + (size_t)wrow * g.d + k0 + col
-                               : w + (size_t)g.f * g.d + (size_t)wrow * g.d + k0 + col;
-        } else {
-            asrc[i] = g.a + (size_t)(row0 + rr) * g.f + k0 + col;
-            const uint16_t *w2 = reinterpret_cast<const uint16_t *>(slab) + (size_t)2 * g.f * g.d;
-            bsrc[i] = w2 + (size_t)(nt * kBRows + r) * g.f + k0 + col;
-        }
+        const int rr = r < rows ? r : 0;
+        if (kGateUp) asrc[i] = g.a + (size_t)(g.perm[row0 + rr] / g.k) * g.d + k0 + col;
+        else asrc[i] = g.a + (size_t)(row0 + rr) * g.f + k0 + col;
     }
 
-    u32x4_t ra[4], rb[4];
-#define MOE_FETCH1(i, ko)                                                                                 \
-    ra[i] = avalid[i] ? *reinterpret_cast<const u32x4_t *>(asrc[i] + (ko)) : u32x4_t{0, 0, 0, 0};       \
-    rb[i] = *reinterpret_cast<const u32x4_t *>(bsrc[i] + (ko));
-#define MOE_FETCH(step)                                                                                   \
-    do {                                                                                                  \
-        const int ko_ = (step) * kBK;                                                                     \
-        MOE_FETCH1(0, ko_) MOE_FETCH1(1, ko_) MOE_FETCH1(2, ko_) MOE_FETCH1(3, ko_)                       \
+    u32x4_t ra[kS][kANum], rb[kS][kNB * kKBlocks];
+    floatx4_t acc[kMBlocks][kNB];
+#pragma unroll
+    for (int m = 0; m < kMBlocks; ++m)
+#pragma unroll
+        for (int nb = 0; nb < kNB; ++nb) acc[m][nb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+
+#define MOE_LOAD(set, step)                                                                           \
+    do {                                                                                              \
+        const int ko_ = min((step), nsteps - 1) * kBK;                                                \
+        _Pragma("unroll") for (int i = 0; i < kANum; ++i) ra[set][i] =                                \
+            *reinterpret_cast<const u32x4_t *>(asrc[i] + ko_);                                        \
+        _Pragma("unroll") for (int nb = 0; nb < kNB; ++nb)                                            \
+        _Pragma("unroll") for (int kb = 0; kb < kKBlocks; ++kb) rb[set][nb * kKBlocks + kb] =         \
+            *reinterpret_cast<const u32x4_t *>(bsrc[nb] + ko_ + 32 * kb);                             \
     } while (0)
-#define MOE_STASH1(i, buf)                                                                                \
-    {                                                                                                     \
-        const int c_ = tid + kThreads * (i);                                                              \
-        const int o_ = (c_ >> 3) * kLdsStride + (c_ & 7) * 8;                                             \
-        *reinterpret_cast<u32x4_t *>(&lds_a[(buf)][o_]) = ra[i];                                          \
-        *reinterpret_cast<u32x4_t *>(&lds_b[(buf)][o_]) = rb[i];                                          \
-    }
-#define MOE_STASH(buf)                                                                                    \
-    do {                                                                                                  \
-        MOE_STASH1(0, buf) MOE_STASH1(1, buf) MOE_STASH1(2, buf) MOE_STASH1(3, buf)                       \
+#define MOE_STASH(set, buf)                                                                           \
+    do {                                                                                              \
+        _Pragma("unroll") for (int i = 0; i < kANum; ++i) {                                           \
+            const int c_ = tid + kGThreads * i;                                                       \
+            *reinterpret_cast<u32x4_t *>(&lds_a[buf][(c_ >> 3) * kLdsStride + (c_ & 7) * 8]) = ra[set][i]; \
+        }                                                                                             \
+    } while (0)
+#define MOE_MMA(set, buf)                                                                             \
+    do {                                                                                              \
+        _Pragma("unroll") for (int kb = 0; kb < kKBlocks; ++kb) {                                     \
+            _Pragma("unroll") for (int m = 0; m < kMBlocks; ++m) {                                    \
+                const bf16x8_t a_ = *reinterpret_cast<const bf16x8_t *>(                              \
+                    &lds_a[buf][(m * 16 + (lane & 15)) * kLdsStride + kb * 32 + 8 * (lane >> 4)]);    \
+                _Pragma("unroll") for (int nb = 0; nb < kNB; ++nb) acc[m][nb] =                       \
+                    __builtin_amdgcn_mfma_f32_16x16x32_bf16(                                          \
+                        a_, __builtin_bit_cast(bf16x8_t, rb[set][nb * kKBlocks + kb]), acc[m][nb], 0, 0, 0); \
+            }                                                                                         \
+        }                                                                                             \
     } while (0)
 
-    const int lane = tid & 63, wv = tid >> 6;
-    const int wm = wv >> 1, wn = wv & 1;
-    // B rows of this wave: gate/up -> gate rows wn*32.. and up rows 64+wn*32..;
-    // down -> rows wn*64 .. +64 (two 32-row blocks).
-    const int brow0 = kGateUp ? wn * 32 : wn * 64;
-    const int brow1 = kGateUp ? 64 + wn * 32 : wn * 64 + 32;
-    floatx16_t acc[2][2];
 #pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < 2; ++b)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
-
-    MOE_FETCH(0);
-    MOE_STASH(0);
+    for (int p = 0; p < kS - 1; ++p) MOE_LOAD(p, p);
+    MOE_STASH(0, 0);
     __syncthreads();
-    for (int s = 0; s < nsteps; ++s) {
-        const int buf = s & 1;
-        if (s + 1 < nsteps) MOE_FETCH(s + 1);
+    for (int s = 0; s < nsteps; s += kS) {
 #pragma unroll
-        for (int kk = 0; kk < kBK / 16; ++kk) {
-            const int kc = kk * 16 + 8 * (lane >> 5);
-            bf16x8_t af[2], bfr[2];
-#pragma unroll
-            for (int a = 0; a < 2; ++a)
-                af[a] = *reinterpret_cast<const bf16x8_t *>(&lds_a[buf][(wm * 64 + a * 32 + (lane & 31)) * kLdsStride + kc]);
-            bfr[0] = *reinterpret_cast<const bf16x8_t *>(&lds_b[buf][(brow0 + (lane & 31)) * kLdsStride + kc]);
-            bfr[1] = *reinterpret_cast<const bf16x8_t *>(&lds_b[buf][(brow1 + (lane & 31)) * kLdsStride + kc]);
-#pragma unroll
-            for (int a = 0; a < 2; ++a)
-#pragma unroll
-                for (int b = 0; b < 2; ++b)
-                    acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bfr[b], acc[a][b], 0, 0, 0);
-        }
-        if (s + 1 < nsteps) {
-            MOE_STASH(buf ^ 1);
+        for (int u = 0; u < kS; ++u) {
+            if (s + u >= nsteps) break;
+            MOE_LOAD((u + kS - 1) % kS, s + u + kS - 1);
+            MOE_MMA(u, (s + u) & 1);
+            MOE_STASH((u + 1) % kS, (s + u + 1) & 1);
             __syncthreads();
         }
     }
-#undef MOE_FETCH
-#undef MOE_FETCH1
+#undef MOE_LOAD
 #undef MOE_STASH
-#undef MOE_STASH1
+#undef MOE_MMA
 
-    // Epilogue. Output element r of a 32x32 block sits at row 8*(r/4) + 4*(lane/32) + r%4,
-    // column lane%32.
+    // Output element r of a 16x16 block sits at row 4*(lane/16) + r, column lane%16.
+    const int P = g.off[g.n];
 #pragma unroll
-    for (int a = 0; a < 2; ++a) {
+    for (int m = 0; m < kMBlocks; ++m) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const int tr = wm * 64 + a * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        for (int r = 0; r < 4; ++r) {
+            const int tr = m * 16 + 4 * (lane >> 4) + r;
             if (tr >= rows) continue;
-            const size_t prow = (size_t)(row0 + tr);
             if (kGateUp) {
-                const float gv = acc[a][0][r], uv = acc[a][1][r];
+                const float gv = acc[m][0][r], uv = acc[m][1][r];
                 const float hv = gv / (1.0f + expf(-gv)) * uv;
-                g.h[prow * g.f + nt * 64 + wn * 32 + (lane & 31)] = f2bf(hv);
+                g.h[(size_t)(row0 + tr) * g.f + nt * 128 + wv * 16 + (lane & 15)] = f2bf(hv);
             } else {
-                const int P = g.off[g.n];
-                float *dst = g.yp + ((size_t)ks * P + prow) * g.d + nt * kBRows;
-                dst[wn * 64 + (lane & 31)] = acc[a][0][r];
-                dst[wn * 64 + 32 + (lane & 31)] = acc[a][1][r];
+                float *dst = g.yp + ((size_t)ks * P + row0 + tr) * g.d + nt * (kGWaves * 16 * kNB) + wv * 16 * kNB +
+                             (lane & 15);
+#pragma unroll
+                for (int nb = 0; nb < kNB; ++nb) dst[16 * nb] = acc[m][nb][r];
             }
         }
     }
 }
 
-// OUT[t][i] = sum_r w[t][r] * sum_s Yp[s][pos[t*k+r]][i]
+// OUT[t][i] = sum_r w[t][r] * sum_s Yp[s][pos[t*k+r]][i], four consecutive i per thread;
+// work group b covers token b / nparts, columns (b mod nparts) * 1024 ...
 __global__ __launch_bounds__(kThreads) void k_prefill_combine(const float *yp, const int32_t *pos, const float *w,
-                                                              int k, int d, int P, int ksplit, float *out)
+                                                              int k, int d, int P, int ksplit, int nparts, float *out)
 {
-    const int t = blockIdx.x;
-    for (int i = threadIdx.x; i < d; i += kThreads) {
-        float acc = 0.f;
-        for (int r = 0; r < k; ++r) {
-            const int pr = pos[t * k + r];
-            float s = 0.f;
-            for (int q = 0; q < ksplit; ++q) s += yp[((size_t)q * P + pr) * d + i];
-            acc = fmaf(w[t * k + r], s, acc);
+    const int t = blockIdx.x / nparts;
+    const int i = ((blockIdx.x % nparts) * kThreads + threadIdx.x) * 4;
+    if (i >= d) return;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int r = 0; r < k; ++r) {
+        const int pr = pos[t * k + r];
+        float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int q = 0; q < ksplit; ++q) {
+            const float4 v = *reinterpret_cast<const float4 *>(yp + ((size_t)q * P + pr) * d + i);
+            s.x += v.x;
+            s.y += v.y;
+            s.z += v.z;
+            s.w += v.w;
         }
-        out[(size_t)t * d + i] = acc;
+        const float wr = w[t * k + r];
+        acc.x = fmaf(wr, s.x, acc.x);
+        acc.y = fmaf(wr, s.y, acc.y);
+        acc.z = fmaf(wr, s.z, acc.z);
+        acc.w = fmaf(wr, s.w, acc.w);
     }
+    *reinterpret_cast<float4 *>(out + (size_t)t * d + i) = acc;
 }
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+// K splits of the down GEMM: four when each part is still a whole number of K steps.
+int down_splits(int f) { return f % (kMaxDownSplits * kBK) == 0 ? kMaxDownSplits : 2; }
 
 struct PrefillWs {
     uint16_t *xb;
@@ -312,7 +344,7 @@ size_t layout(int d, int f, int n, int k, int T, uint8_t *base, PrefillWs *ws)
     uint8_t *perm = take(P * 4);
     uint8_t *pos = take(P * 4);
     uint8_t *h = take(P * f * 2);
-    uint8_t *yp = take((size_t)kDownSplits * P * d * 4);
+    uint8_t *yp = take((size_t)kMaxDownSplits * P * d * 4);
     if (ws) {
         ws->xb = reinterpret_cast<uint16_t *>(xb);
         ws->idx = reinterpret_cast<int32_t *>(idx);
@@ -341,7 +373,7 @@ hipError_t launch_prefill(const PrefillPlan &P, const float *X, float *OUT, int3
     if ((e = launch_router(X, P.wr, P.T, P.d, P.n, P.k, idx_d, w_d, s)) != hipSuccess) return e;
     const int npairs = P.T * P.k;
     (void)hipGetLastError();
-    hipLaunchKernelGGL(k_group, dim3(1), dim3(kThreads), 0, s, idx_d, npairs, P.n, ws.off, ws.perm, ws.pos);
+    hipLaunchKernelGGL(k_group, dim3(1), dim3(kGroupThreads), 0, s, idx_d, npairs, P.n, ws.off, ws.perm, ws.pos);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     const int64_t n8 = (int64_t)P.T * P.d / 8;
     const int cast_blocks = (int)std::min<int64_t>((n8 + kThreads - 1) / kThreads, 4096);
@@ -357,29 +389,32 @@ hipError_t launch_prefill(const PrefillPlan &P, const float *X, float *OUT, int3
     g.k = P.k;
     g.d = P.d;
     g.f = P.f;
-    g.mtiles = (P.T + kBM - 1) / kBM;
+    g.mtiles = (P.T + kTileM - 1) / kTileM;
     g.h = ws.h;
     g.yp = ws.yp;
     const int groups = (P.n + kXcds - 1) / kXcds;
 
-    // gate/up: N tiles of 64 rows per matrix over f, K = d
+    // gate/up: each work group covers 128 columns of H (128 W1 rows + the same 128 W3 rows), K = d
     g.a = ws.xb;
-    g.ntiles = P.f / 64;
+    g.ntiles = P.f / 128;
     g.ksplit = 1;
     g.per_xcd = groups * g.mtiles * g.ntiles * g.ksplit;
-    hipLaunchKernelGGL(k_group_gemm<true>, dim3(kXcds * g.per_xcd), dim3(kThreads), 0, s, g);
+    hipLaunchKernelGGL((k_moe_gemm<true, 3, 2>), dim3(kXcds * g.per_xcd), dim3(kGThreads), 0, s, g);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
-    // down: N tiles of 128 output rows over d, K = f split in two
+    // down: 256 (or 128) output rows per work group, K = f split in 4 (or 2) parts
     g.a = ws.h;
-    g.ntiles = P.d / kBRows;
-    g.ksplit = kDownSplits;
+    g.ksplit = down_splits(P.f);
+    const bool wide = P.d % 256 == 0;
+    g.ntiles = P.d / (wide ? 256 : 128);
     g.per_xcd = groups * g.mtiles * g.ntiles * g.ksplit;
-    hipLaunchKernelGGL(k_group_gemm<false>, dim3(kXcds * g.per_xcd), dim3(kThreads), 0, s, g);
+    if (wide) hipLaunchKernelGGL((k_moe_gemm<false, 4, 2>), dim3(kXcds * g.per_xcd), dim3(kGThreads), 0, s, g);
+    else hipLaunchKernelGGL((k_moe_gemm<false, 4, 1>), dim3(kXcds * g.per_xcd), dim3(kGThreads), 0, s, g);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
-    hipLaunchKernelGGL(k_prefill_combine, dim3(P.T), dim3(kThreads), 0, s, ws.yp, ws.pos, w_d, P.k, P.d, npairs,
-                       kDownSplits, OUT);
+    const int nparts = (P.d + 4 * kThreads - 1) / (4 * kThreads);
+    hipLaunchKernelGGL(k_prefill_combine, dim3(P.T * nparts), dim3(kThreads), 0, s, ws.yp, ws.pos, w_d, P.k, P.d,
+                       npairs, g.ksplit, nparts, OUT);
     return hipGetLastError();
 }
 

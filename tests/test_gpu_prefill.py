@@ -53,8 +53,12 @@ def _pool_np(torch, slabs, d, f):
     return pool.cuda()
 
 
+# (256, 512, 4, 2, 700): 1400 pairs (two chunks of the grouping sort) and ~350 tokens per
+# expert (two 192-token tiles); (384, 640, ...): d not a multiple of 256 (128-row down tiles)
+# and f not a multiple of 256 (two K splits).
 @pytest.mark.parametrize("d,f,n,k,T", [(256, 512, 4, 2, 64), (256, 512, 4, 2, 37), (512, 1024, 8, 2, 300),
-                                       (384, 640, 16, 4, 130), (256, 256, 8, 1, 1), (256, 512, 64, 8, 48)])
+                                       (384, 640, 16, 4, 130), (256, 256, 8, 1, 1), (256, 512, 64, 8, 48),
+                                       (256, 512, 4, 2, 700)])
 def test_prefill_small(d, f, n, k, T):
     torch = torch_cuda()
     say("prefill", d, f, n, k, T)
