@@ -184,12 +184,13 @@ __global__ __launch_bounds__(kGThreads) void k_moe_gemm(GemmArgs g)
     const int k0 = ks * kspan;
     const int nsteps = kspan / kBK;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+    const int nmb = (rows + 15) >> 4;                  // token blocks holding tokens of this tile
     const uint16_t *w = reinterpret_cast<const uint16_t *>(g.pool + (uint64_t)e * g.slab_stride);
 
     static_assert(!kGateUp || kNB == 2, "gate/up pairs a W1 block with a W3 block");
     // this lane's weight rows (MFMA column lane mod 16 of each column block) and K offset
     const uint16_t *bsrc[kNB];
-    if (kGateUp) {
+    if constexpr (kGateUp) {
         const size_t wrow = (size_t)nt * 128 + wv * 16 + (lane & 15);
         bsrc[0] = w + wrow * g.d + k0 + 8 * (lane >> 4);
         bsrc[1] = w + (size_t)g.f * g.d + wrow * g.d + k0 + 8 * (lane >> 4);
@@ -238,11 +239,13 @@ __global__ __launch_bounds__(kGThreads) void k_moe_gemm(GemmArgs g)
     do {                                                                                              \
         _Pragma("unroll") for (int kb = 0; kb < kKBlocks; ++kb) {                                     \
             _Pragma("unroll") for (int m = 0; m < kMBlocks; ++m) {                                    \
-                const bf16x8_t a_ = *reinterpret_cast<const bf16x8_t *>(                              \
-                    &lds_a[buf][(m * 16 + (lane & 15)) * kLdsStride + kb * 32 + 8 * (lane >> 4)]);    \
-                _Pragma("unroll") for (int nb = 0; nb < kNB; ++nb) acc[m][nb] =                       \
-                    __builtin_amdgcn_mfma_f32_16x16x32_bf16(                                          \
-                        a_, __builtin_bit_cast(bf16x8_t, rb[set][nb * kKBlocks + kb]), acc[m][nb], 0, 0, 0); \
+                if (m < nmb) {                                                                        \
+                    const bf16x8_t a_ = *reinterpret_cast<const bf16x8_t *>(                          \
+                        &lds_a[buf][(m * 16 + (lane & 15)) * kLdsStride + kb * 32 + 8 * (lane >> 4)]); \
+                    _Pragma("unroll") for (int nb = 0; nb < kNB; ++nb) acc[m][nb] =                   \
+                        __builtin_amdgcn_mfma_f32_16x16x32_bf16(                                      \
+                            a_, __builtin_bit_cast(bf16x8_t, rb[set][nb * kKBlocks + kb]), acc[m][nb], 0, 0, 0); \
+                }                                                                                     \
             }                                                                                         \
         }                                                                                             \
     } while (0)
@@ -273,8 +276,8 @@ __global__ __launch_bounds__(kGThreads) void k_moe_gemm(GemmArgs g)
         for (int r = 0; r < 4; ++r) {
             const int tr = m * 16 + 4 * (lane >> 4) + r;
             if (tr >= rows) continue;
-            if (kGateUp) {
-                const float gv = acc[m][0][r], uv = acc[m][1][r];
+            if constexpr (kGateUp) {
+                const float gv = acc[m][0][r], uv = acc[m][kNB - 1][r];
                 const float hv = gv / (1.0f + expf(-gv)) * uv;
                 g.h[(size_t)(row0 + tr) * g.f + nt * 128 + wv * 16 + (lane & 15)] = f2bf(hv);
             } else {
@@ -399,7 +402,7 @@ hipError_t launch_prefill(const PrefillPlan &P, const float *X, float *OUT, int3
     g.ntiles = P.f / 128;
     g.ksplit = 1;
     g.per_xcd = groups * g.mtiles * g.ntiles * g.ksplit;
-    hipLaunchKernelGGL((k_moe_gemm<true, 3, 2>), dim3(kXcds * g.per_xcd), dim3(kGThreads), 0, s, g);
+    hipLaunchKernelGGL((k_moe_gemm<true, 2, 2>), dim3(kXcds * g.per_xcd), dim3(kGThreads), 0, s, g);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     // down: 256 (or 128) output rows per work group, K = f split in 4 (or 2) parts
