@@ -32,7 +32,7 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def build_world(torch, moe, synth, wl, steps_total, seed, threads, pinned_gb):
+def build_world(torch, moe, synth, wl, steps_total, seed, threads, pinned_gb, policy="lru", budget_gb=None):
     """Device cache, pinned host experts, router weights and hidden states.
 
     Page-locked host memory is capped per process on the GPU hosts (64 GiB), below
@@ -68,14 +68,22 @@ def build_world(torch, moe, synth, wl, steps_total, seed, threads, pinned_gb):
                       for l in range(L)]).contiguous()
     X = np.stack([synth.ar1_states(synth.seed_for(seed, wl.name, "states", l), steps_total, d) for l in range(L)])
     xd = torch.from_numpy(np.ascontiguousarray(X.transpose(1, 0, 2))).cuda()     # [T, L, d]
-    pool = torch.zeros(L * M * stride, dtype=torch.uint8, device="cuda")
-    cache = moe.Cache(L, n, M, k)
+    covered = L
+    if budget_gb is not None:   # Section III-B: slots S = budget / expert size, N = S / M covered layers
+        _, covered = moe.cache_geometry(int(budget_gb * 1e9), stride, M, L)
+    content = None
+    if policy == "static":      # the "random" policy: a seeded uniform M-subset per layer, fixed
+        content = [sorted(np.random.default_rng(synth.seed_for(seed, wl.name, "static-content", l))
+                          .choice(n, M, replace=False).tolist()) for l in range(covered)]
+    pool = torch.zeros(covered * M * stride, dtype=torch.uint8, device="cuda") if covered else None
+    cache = moe.Cache(covered, n, M, k, policy=policy, static_content=content)
     hp = moe.HostPool(threads)
     rt = moe.Runtime(d, f, n, k, M, L, wr, pool, host_addrs, cache, hp, f_shared=wl.f_shared, shared_pool=shared)
     torch.cuda.synchronize()
-    log(f"world ready in {time.perf_counter() - t0:.1f}s (device cache {pool.numel() / 1e9:.1f} GB)")
+    log(f"world ready in {time.perf_counter() - t0:.1f}s (device cache {0 if pool is None else pool.numel() / 1e9:.1f} GB, "
+        f"{covered} of {L} layers covered, policy {policy})")
     return dict(hosts=hosts, H=H, wr=wr, X=X, xd=xd, pool=pool, shared=shared, cache=cache, hp=hp, rt=rt,
-                stride=stride)
+                stride=stride, covered=covered, policy=policy)
 
 
 def cpu_baseline(wl, world, seed, budget_s, t_first):
@@ -144,6 +152,65 @@ def host_sweep(moe, wl, world, threads_list=(1, 2, 4, 8, 16)):
         ms = sorted(times)[1] * 1e3
         out[str(t)] = {"ms": round(ms, 2), "GB/s": round(k * 3 * d * f * 2 / (ms * 1e-3) / 1e9, 1)}
     return out
+
+
+def hit_study(args, torch, moe, synth, wl):
+    """Cache hit rates by policy and ways (the analog of the paper's Fig. on cache
+    configurations and eviction policies, Section IV-D): the GPU router selects the
+    experts of every AR(1) token of every layer, and the library's cache replays
+    those selections under LRU, FIFO and a static random content. Also i.i.d. uniform
+    selections, whose long-run rates must match the closed forms for every policy."""
+    import math
+    import numpy as np
+    d, n, k, L, T = wl.d, wl.n, wl.k, wl.L, wl.T
+    wr = torch.stack([synth.router_weights_torch(synth.seed_for(args.seed, wl.name, "router", l), n, d)
+                      for l in range(L)]).contiguous()
+    sel = np.empty((L, T, k), np.int32)
+    for l in range(L):
+        X = torch.from_numpy(synth.ar1_states(synth.seed_for(args.seed, wl.name, "states", l), T, d)).cuda()
+        idx, _ = moe.router_topk(X, wr[l], k)
+        sel[l] = idx.cpu().numpy()
+    rng = np.random.default_rng(synth.seed_for(args.seed, wl.name, "subsets"))
+    iid = np.stack([np.stack([rng.choice(n, k, replace=False) for _ in range(T)]) for _ in range(L)]).astype(np.int32)
+    ways_list = sorted({m for m in (k, 2 * k, n // 4, n // 2, 3 * n // 4, wl.ways) if k <= m < n})
+
+    def replay(trace, policy, M, warm):
+        content = None
+        if policy == "static":
+            content = [sorted(np.random.default_rng(synth.seed_for(args.seed, wl.name, "static-content", l))
+                              .choice(n, M, replace=False).tolist()) for l in range(L)]
+        c = moe.Cache(L, n, M, k, policy=policy, static_content=content)
+        anyh = allh = eh = ev = 0
+        for t in range(T):
+            for l in range(L):
+                _, hits = c.lookup(l, trace[l, t])
+                c.update(l, trace[l, t])
+                if t >= warm:
+                    anyh += bool(hits.any())
+                    allh += bool(hits.all())
+                    eh += int(hits.sum())
+                    ev += 1
+        return {"any_hit": round(anyh / ev, 4), "all_hit": round(allh / ev, 4), "expert_hit": round(eh / (ev * k), 4)}
+
+    rows = []
+    for M in ways_list:
+        row = {"ways": M,
+               "closed_form": {"any_hit": round(1 - math.comb(n - M, k) / math.comb(n, k), 4),
+                               "all_hit": round(math.comb(M, k) / math.comb(n, k), 4)}}
+        for policy in ("lru", "fifo", "static"):
+            row[policy] = replay(sel, policy, M, warm=8)
+            row["iid_" + policy] = replay(iid, policy, M, warm=8)
+        rows.append(row)
+        log(json.dumps(row))
+    return {
+        "metric": "expert-cache hit rate by policy and ways (router selections of AR(1) hidden states)",
+        "value": next(r["lru"]["expert_hit"] for r in rows if r["ways"] == wl.ways) if wl.ways in ways_list else None,
+        "unit": "fraction of selected experts found in the cache (LRU, the workload's ways)",
+        "n_gpus": 1, "higher_is_better": True, "data": "synthetic",
+        "config": {"workload": wl.desc, "experts": n, "top_k": k, "layers": L, "tokens": T,
+                   "warm_tokens_excluded": 8, "events_per_row": L * (T - 8)},
+        "rows": rows,
+    }
 
 
 def measured_traffic(args):
@@ -239,6 +306,12 @@ def main():
     ap.add_argument("--pinned-gb", type=float, default=56.0, help="page-locked host memory for expert copies (GiB)")
     ap.add_argument("--cpu-baseline-s", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--policy", default="lru", choices=["lru", "fifo", "static"],
+                    help="cache replacement policy (Section IV-D; the paper's is LRU)")
+    ap.add_argument("--budget-gb", type=float, default=None,
+                    help="GPU memory for the expert cache (GB); layers past the covered ones run on the host")
+    ap.add_argument("--hit-study", action="store_true",
+                    help="only replay router selections through LRU/FIFO/static caches of several sizes")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB 5 times (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -264,12 +337,16 @@ def main():
         print(json.dumps({"copy_calibration_bytes_read": nbytes, "copy_calibration_bytes_written": nbytes}))
         return
     wl = synth.WORKLOADS[args.workload]
+    if args.hit_study:
+        print(json.dumps(hit_study(args, torch, moe, synth, wl)), flush=True)
+        return
     if wl.prefill:
         print(json.dumps(bench_prefill(args, torch, moe, synth, wl)), flush=True)
         return
     steps_total = args.warmup + args.steps
     assert steps_total <= wl.T, f"at most {wl.T} decode steps in this workload"
-    world = build_world(torch, moe, synth, wl, steps_total, args.seed, args.threads, args.pinned_gb)
+    world = build_world(torch, moe, synth, wl, steps_total, args.seed, args.threads, args.pinned_gb,
+                        policy=args.policy, budget_gb=args.budget_gb)
     rt, xd = world["rt"], world["xd"]
     L, k, d = wl.L, wl.k, wl.d
     out = torch.empty((2, L, d), dtype=torch.float32, device="cuda")
@@ -323,6 +400,7 @@ def main():
             "weights": "bf16, fp32 accumulate", "cache_start": f"cold, {args.warmup} warmup tokens",
             "host_threads": world["hp"].threads, "parallelism": "single GPU",
             "host_expert_layers_distinct": world["H"],
+            "cache_policy": world["policy"], "covered_layers": world["covered"],
         },
         "roofline": {
             "kernel": "k_gate_up (W1/W3 rows + SiLU*mul)",

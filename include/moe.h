@@ -77,7 +77,7 @@ int moe_router_topk(const float *x, const float *w_router, int T, int d, int n, 
                     int32_t *idx_out, float *w_out, void *stream);
 
 /* ------------------------------------------------------------------------- */
-/* Expert cache: N-index (one per layer), M-way, LRU (Section III-B).         */
+/* Expert cache: N-index (one per layer), M-way (Section III-B).             */
 /* ------------------------------------------------------------------------- */
 /*
  * Host-side slot table. Each layer owns one set of `ways` slots, initially empty.
@@ -90,11 +90,39 @@ int moe_router_topk(const float *x, const float *w_router, int T, int d, int n, 
  */
 typedef struct moe_cache moe_cache;
 
-/* EINVAL unless 1 <= top_k <= ways <= n_experts <= MOE_MAX_EXPERTS, n_layers >= 1. */
+/* LRU cache. EINVAL unless 1 <= top_k <= ways <= n_experts <= MOE_MAX_EXPERTS, n_layers >= 1. */
 int moe_cache_create(int n_layers, int n_experts, int ways, int top_k, moe_cache **out);
+
+/*
+ * Replacement policies compared in Section IV-D:
+ *   MOE_POLICY_LRU    the paper's policy (above);
+ *   MOE_POLICY_FIFO   as LRU, except that a hit does not refresh its slot, so the victim
+ *                     is the earliest-inserted slot whose expert is not selected;
+ *   MOE_POLICY_STATIC the paper's "random" policy: each set holds a fixed content of
+ *                     `ways` experts for ever; misses are never inserted (no post-fetch).
+ */
+#define MOE_POLICY_LRU 0
+#define MOE_POLICY_FIFO 1
+#define MOE_POLICY_STATIC 2
+/*
+ * Cache with a policy. n_layers >= 0 sets (the covered layers; a runtime with more
+ * layers runs the others entirely on the host). static_content: host int32
+ * [n_layers][ways], distinct expert ids per layer, required for MOE_POLICY_STATIC
+ * (the caller draws it, e.g. uniformly at random) and ignored otherwise; it is
+ * copied. LRU/FIFO need top_k <= ways <= n_experts; STATIC needs 1 <= ways <= n_experts.
+ */
+int moe_cache_create_policy(int n_layers, int n_experts, int ways, int top_k, int policy,
+                            const int32_t *static_content, moe_cache **out);
 void moe_cache_destroy(moe_cache *c);
-/* Empties every set (cold cache). */
+/* Back to the initial state: every set empty (LRU, FIFO) or the static content. */
 int moe_cache_reset(moe_cache *c);
+/*
+ * Cache geometry from a memory budget (Section III-B): slots S = floor(budget_bytes /
+ * expert_bytes), indexes N = floor(S / ways); covered_out = min(N, n_layers), the
+ * layers 0..covered-1 that own a set. Either output may be NULL.
+ */
+int moe_cache_geometry(size_t budget_bytes, size_t expert_bytes, int ways, int n_layers,
+                       int *slots_out, int *covered_out);
 /*
  * Step 1 (cache check), pure. experts: host [k] distinct ids in [0, n).
  * slot_out: host [k] slot holding each expert, -1 on a miss; hit_out: host [k] 0/1.
@@ -177,13 +205,15 @@ typedef struct moe_layer_desc {
     int d, f;            /* d_model, d_ffn of a routed expert */
     int n, k;            /* experts per layer, experts per token */
     int ways;            /* cache slots per layer (M) */
-    int n_layers;        /* layers (one cache set each) */
+    int n_layers;        /* layers; the first cache->n_layers own a cache set, the rest
+                            (uncovered, Section III-B) run every expert on the host */
     int f_shared;        /* d_ffn of an always-active shared expert, 0 = none */
     const float *w_router;       /* device fp32 [n_layers][n][d] */
-    void *slot_pool;             /* device, n_layers*ways slabs (layer-major), stride moe_slab_bytes(d,f) */
+    void *slot_pool;             /* device, covered*ways slabs (layer-major), stride moe_slab_bytes(d,f);
+                                    may be NULL when no layer is covered */
     const void *shared_pool;     /* device, n_layers slabs of moe_slab_bytes(d,f_shared), or NULL */
     const void *const *host_slabs; /* host array of n_layers*n pointers to pinned host slabs (copied at create) */
-    moe_cache *cache;            /* n_layers sets, `ways` ways, top_k == k (borrowed) */
+    moe_cache *cache;            /* covered <= n_layers sets, `ways` ways, top_k == k (borrowed) */
     moe_host_pool *pool;         /* host thread pool (borrowed) */
 } moe_layer_desc;
 
@@ -191,9 +221,9 @@ typedef struct moe_runtime moe_runtime;
 
 /*
  * Allocates at creation (never per token): device workspace, device expert->slot
- * mirror [n_layers][n] (all -1), pinned staging, events. The slot pool must be
- * consistent with the cache: slots the cache holds contain those experts' slabs
- * (a fresh cache is empty, so any pool content is consistent).
+ * mirror [n_layers][n], pinned staging, events. Slots the cache already holds at
+ * creation (a static content, a warm cache) are filled from the host slabs then,
+ * synchronously, so the pool is consistent with the cache.
  */
 int moe_runtime_create(const moe_layer_desc *desc, moe_runtime **out);
 void moe_runtime_destroy(moe_runtime *rt);

@@ -18,6 +18,15 @@ Points the paper leaves open, and the reading taken here:
 `LRUSet` is that procedure. `definitional_hits` is an independent statement of the
 same policy (content = the M experts with the most recent use keys) and
 `textbook_lru_hits` is classic single-reference LRU (stack distance < M) for k = 1.
+
+Section IV-D compares LRU with two other policies, modelled here the same way:
+  * `FIFOSet`: first in, first out -- identical to `LRUSet` except that a hit does
+    not refresh its slot, so the victim is the earliest-inserted slot whose expert
+    is not selected by the current token;
+  * `StaticSet` (the paper's "random" policy): a fixed set of M experts chosen once
+    (the caller draws it, e.g. uniformly at random, and passes it in); misses are
+    never inserted, so the content never changes.
+`textbook_fifo_hits` is classic single-reference FIFO for k = 1.
 """
 from __future__ import annotations
 
@@ -81,11 +90,72 @@ class LRUSet:
         return slots, hits, fills, evicted
 
 
-class LRUCache:
-    """The N-index (one index per layer), M-way cache."""
+class FIFOSet(LRUSet):
+    """One set with first-in-first-out replacement: a hit leaves the stamps alone,
+    so a slot's stamp is the clock of its insertion."""
 
-    def __init__(self, n_layers: int, ways: int):
-        self.sets = [LRUSet(ways) for _ in range(n_layers)]
+    def access(self, selected: Sequence[int]):
+        sel = list(selected)
+        if len(set(sel)) != len(sel):
+            raise ValueError("selected experts must be distinct")
+        if len(sel) > self.ways:
+            raise ValueError("more selected experts than ways")
+        slots, hits = self.lookup(sel)
+        hit_of = dict(zip(sel, hits))
+        current = set(sel)
+        fill_of, evict_of = {}, {}
+        for e in sorted(sel):
+            self.clock += 1
+            if hit_of[e]:
+                continue                      # no refresh: insertion order decides
+            empty = [s for s in range(self.ways) if self.expert[s] < 0]
+            if empty:
+                victim = empty[0]
+            else:
+                candidates = [s for s in range(self.ways) if self.expert[s] not in current]
+                victim = min(candidates, key=lambda s: self.stamp[s])
+            fill_of[e] = victim
+            evict_of[e] = self.expert[victim]
+            self.expert[victim] = e
+            self.stamp[victim] = self.clock
+        fills = [fill_of.get(e, -1) for e in sel]
+        evicted = [evict_of.get(e, -1) for e in sel]
+        return slots, hits, fills, evicted
+
+
+class StaticSet(LRUSet):
+    """One set whose content is fixed: slot s holds content[s] forever."""
+
+    def __init__(self, ways: int, content: Sequence[int]):
+        super().__init__(ways)
+        content = list(content)
+        if len(content) != ways or len(set(content)) != ways or min(content) < 0:
+            raise ValueError("static content must be `ways` distinct expert ids")
+        self.expert = content
+
+    def access(self, selected: Sequence[int]):
+        sel = list(selected)
+        if len(set(sel)) != len(sel):
+            raise ValueError("selected experts must be distinct")
+        slots, hits = self.lookup(sel)
+        return slots, hits, [-1] * len(sel), [-1] * len(sel)
+
+
+POLICIES = {"lru": LRUSet, "fifo": FIFOSet}
+
+
+class LRUCache:
+    """The N-index (one index per layer), M-way cache.
+
+    policy "lru" (the paper's), "fifo", or "static" with `static_content[layer]`
+    giving each covered layer's M experts. Only layers 0..n_layers-1 own a set.
+    """
+
+    def __init__(self, n_layers: int, ways: int, policy: str = "lru", static_content=None):
+        if policy == "static":
+            self.sets = [StaticSet(ways, static_content[l]) for l in range(n_layers)]
+        else:
+            self.sets = [POLICIES[policy](ways) for _ in range(n_layers)]
 
     def access(self, layer: int, selected: Sequence[int]):
         return self.sets[layer].access(selected)
@@ -131,6 +201,23 @@ def textbook_lru_hits(trace: Iterable[int], ways: int) -> List[bool]:
         else:
             out.append(False)
         hist.append(e)
+    return out
+
+
+def textbook_fifo_hits(trace: Iterable[int], ways: int) -> List[bool]:
+    """Classic FIFO for one reference per step: a queue of at most M items; a miss
+    appends the item and drops the oldest when the queue is over M; a hit changes
+    nothing."""
+    queue: List[int] = []
+    out = []
+    for e in trace:
+        if e in queue:
+            out.append(True)
+            continue
+        out.append(False)
+        queue.append(e)
+        if len(queue) > ways:
+            queue.pop(0)
     return out
 
 

@@ -77,14 +77,24 @@ def router_topk(x, w_router, k, idx_out=None, w_out=None, stream=None):
 
 
 # --------------------------------------------------------------------------- cache
-class Cache:
-    """Host slot table of the per-layer LRU expert cache."""
+POLICIES = {"lru": 0, "fifo": 1, "static": 2}
 
-    def __init__(self, n_layers, n_experts, ways, top_k):
+
+class Cache:
+    """Host slot table of the per-layer expert cache (policy "lru", "fifo" or
+    "static"; `static_content` [n_layers][ways] for "static")."""
+
+    def __init__(self, n_layers, n_experts, ways, top_k, policy="lru", static_content=None):
         h = ctypes.c_void_p()
-        _check("moe_cache_create", _lib.moe_cache_create(n_layers, n_experts, ways, top_k, ctypes.byref(h)))
+        if policy == "static":
+            content = np.ascontiguousarray(static_content, dtype=np.int32).reshape(n_layers, ways)
+            cptr = _np_ptr(content, ctypes.c_int32)
+        else:
+            content, cptr = None, None
+        _check("moe_cache_create_policy", _lib.moe_cache_create_policy(n_layers, n_experts, ways, top_k,
+                                                                       POLICIES[policy], cptr, ctypes.byref(h)))
         self.handle = h
-        self.n_layers, self.n, self.ways, self.k = n_layers, n_experts, ways, top_k
+        self.n_layers, self.n, self.ways, self.k, self.policy = n_layers, n_experts, ways, top_k, policy
 
     def close(self):
         if getattr(self, "handle", None):
@@ -117,6 +127,14 @@ class Cache:
         m = np.empty(self.n, np.int32)
         _check("moe_cache_slotmap", _lib.moe_cache_slotmap(self.handle, layer, _np_ptr(m, ctypes.c_int32)))
         return m
+
+
+def cache_geometry(budget_bytes, expert_bytes, ways, n_layers):
+    """(slots S, covered layers min(N, n_layers)) for a memory budget (Section III-B)."""
+    S, N = ctypes.c_int(), ctypes.c_int()
+    _check("moe_cache_geometry", _lib.moe_cache_geometry(int(budget_bytes), int(expert_bytes), ways, n_layers,
+                                                         ctypes.byref(S), ctypes.byref(N)))
+    return S.value, N.value
 
 
 # --------------------------------------------------------------------------- hit FFN / combine
@@ -203,7 +221,8 @@ def _host_addr(a):
 class Runtime:
     """Per-layer decode runtime (steps 1-3 of the method) over caller-owned buffers.
 
-    w_router: cuda fp32 [L, n, d]; slot_pool: cuda uint8 (L*ways slabs);
+    w_router: cuda fp32 [L, n, d]; slot_pool: cuda uint8 (covered*ways slabs, where
+    covered = cache.n_layers <= L; None when no layer is covered);
     shared_pool: cuda uint8 (L slabs of d x f_shared) or None;
     host_slabs: sequence of L*n host addresses (ints) of pinned bf16 slabs.
     """
@@ -212,7 +231,8 @@ class Runtime:
                  pool: HostPool, f_shared=0, shared_pool=None):
         self._keep = (w_router, slot_pool, shared_pool, cache, pool)
         arr = (ctypes.c_void_p * len(host_slabs))(*[int(a) for a in host_slabs])
-        desc = LayerDesc(d, f, n, k, ways, n_layers, f_shared, w_router.data_ptr(), slot_pool.data_ptr(),
+        desc = LayerDesc(d, f, n, k, ways, n_layers, f_shared, w_router.data_ptr(),
+                         slot_pool.data_ptr() if slot_pool is not None else None,
                          shared_pool.data_ptr() if shared_pool is not None else None,
                          ctypes.cast(arr, ctypes.POINTER(ctypes.c_void_p)), cache.handle, pool.handle)
         h = ctypes.c_void_p()

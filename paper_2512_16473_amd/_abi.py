@@ -50,6 +50,8 @@ SIGNATURES = [
     ("moe_slab_bytes", c_size_t, [c_int, c_int]),
     ("moe_router_topk", c_int, [c_void_p, c_void_p, c_int, c_int, c_int, c_int, c_void_p, c_void_p, c_void_p]),
     ("moe_cache_create", c_int, [c_int, c_int, c_int, c_int, ctypes.POINTER(c_void_p)]),
+    ("moe_cache_create_policy", c_int, [c_int, c_int, c_int, c_int, c_int, c_i32p, ctypes.POINTER(c_void_p)]),
+    ("moe_cache_geometry", c_int, [c_size_t, c_size_t, c_int, c_int, ctypes.POINTER(c_int), ctypes.POINTER(c_int)]),
     ("moe_cache_destroy", None, [c_void_p]),
     ("moe_cache_reset", c_int, [c_void_p]),
     ("moe_cache_lookup", c_int, [c_void_p, c_int, c_i32p, c_int, c_i32p, c_u8p]),

@@ -1,7 +1,10 @@
 // Host-side slot table of the N-index, M-way expert cache (Section III-B):
-// one set per layer, LRU replacement, every missed expert inserted for future
-// tokens (Section III-A step 3).
+// one set per covered layer, LRU replacement with every missed expert inserted for
+// future tokens (Section III-A step 3). Section IV-D's comparison policies are also
+// here: FIFO (a hit does not refresh its slot) and static (a fixed content, misses
+// never inserted).
 #include <algorithm>
+#include <cstdint>
 #include <cstring>
 #include <vector>
 
@@ -27,6 +30,11 @@ void Cache::reset()
     std::fill(slot_used.begin(), slot_used.end(), 0);
     std::fill(tick.begin(), tick.end(), 0);
     std::fill(where.begin(), where.end(), -1);
+    if (policy == MOE_POLICY_STATIC) {
+        slot_expert = initial;
+        for (int l = 0; l < layers; ++l)
+            for (int s = 0; s < ways; ++s) where[(size_t)l * n + initial[(size_t)l * ways + s]] = s;
+    }
 }
 
 void Cache::check(int layer, const int32_t *experts, int k, int32_t *slot_out, uint8_t *hit_out) const
@@ -49,6 +57,13 @@ void Cache::step(int layer, const int32_t *experts, int k, int32_t *fill_out, in
     // Hit status of every selected expert is fixed before any change.
     bool hit[MOE_MAX_TOPK];
     for (int j = 0; j < k; ++j) hit[j] = map[experts[j]] >= 0;
+    if (policy == MOE_POLICY_STATIC) {   // fixed content: nothing is stamped or inserted
+        for (int j = 0; j < k; ++j) {
+            if (fill_out) fill_out[j] = -1;
+            if (evicted_out) evicted_out[j] = -1;
+        }
+        return;
+    }
 
     // Visit the selection in ascending expert id.
     int order[MOE_MAX_TOPK];
@@ -60,7 +75,7 @@ void Cache::step(int layer, const int32_t *experts, int k, int32_t *fill_out, in
         const int32_t e = experts[j];
         ++clk;
         if (hit[j]) {
-            su[map[e]] = clk;
+            if (policy == MOE_POLICY_LRU) su[map[e]] = clk;   // FIFO keeps the insertion stamp
             if (fill_out) fill_out[j] = -1;
             if (evicted_out) evicted_out[j] = -1;
             continue;
@@ -93,30 +108,68 @@ using moe::Cache;
 
 extern "C" {
 
-int moe_cache_create(int n_layers, int n_experts, int ways, int top_k, moe_cache **out)
+int moe_cache_create_policy(int n_layers, int n_experts, int ways, int top_k, int policy,
+                            const int32_t *static_content, moe_cache **out)
 {
     MOE_GUARD_BEGIN
     MOE_REQUIRE(out, "moe_cache_create: null output handle");
-    MOE_REQUIRE(n_layers >= 1, "moe_cache_create: n_layers=%d < 1", n_layers);
+    MOE_REQUIRE(n_layers >= 0, "moe_cache_create: n_layers=%d < 0", n_layers);
     MOE_REQUIRE(n_experts >= 1 && n_experts <= MOE_MAX_EXPERTS, "moe_cache_create: n_experts=%d out of [1,%d]",
                 n_experts, MOE_MAX_EXPERTS);
     MOE_REQUIRE(top_k >= 1 && top_k <= MOE_MAX_TOPK, "moe_cache_create: top_k=%d out of [1,%d]", top_k,
                 MOE_MAX_TOPK);
-    MOE_REQUIRE(ways >= top_k && ways <= n_experts,
-                "moe_cache_create: need top_k <= ways <= n_experts (ways=%d top_k=%d n=%d)", ways, top_k,
-                n_experts);
+    MOE_REQUIRE(policy == MOE_POLICY_LRU || policy == MOE_POLICY_FIFO || policy == MOE_POLICY_STATIC,
+                "moe_cache_create: unknown policy %d", policy);
+    if (policy == MOE_POLICY_STATIC) {
+        MOE_REQUIRE(ways >= 1 && ways <= n_experts, "moe_cache_create: need 1 <= ways <= n_experts (ways=%d n=%d)",
+                    ways, n_experts);
+        MOE_REQUIRE(n_layers == 0 || static_content, "moe_cache_create: the static policy needs its content");
+        for (int l = 0; l < n_layers; ++l)
+            for (int s = 0; s < ways; ++s) {
+                const int32_t e = static_content[(size_t)l * ways + s];
+                MOE_REQUIRE(e >= 0 && e < n_experts, "moe_cache_create: static expert %d (layer %d) out of range", e,
+                            l);
+                for (int q = 0; q < s; ++q)
+                    MOE_REQUIRE(static_content[(size_t)l * ways + q] != e,
+                                "moe_cache_create: expert %d listed twice in layer %d", e, l);
+            }
+    } else {
+        MOE_REQUIRE(ways >= top_k && ways <= n_experts,
+                    "moe_cache_create: need top_k <= ways <= n_experts (ways=%d top_k=%d n=%d)", ways, top_k,
+                    n_experts);
+    }
     Cache *c = new Cache();
     c->layers = n_layers;
     c->n = n_experts;
     c->ways = ways;
     c->top_k = top_k;
+    c->policy = policy;
+    if (policy == MOE_POLICY_STATIC) c->initial.assign(static_content, static_content + (size_t)n_layers * ways);
     c->slot_expert.assign((size_t)n_layers * ways, -1);
     c->slot_used.assign((size_t)n_layers * ways, 0);
     c->tick.assign((size_t)n_layers, 0);
     c->where.assign((size_t)n_layers * n_experts, -1);
+    c->reset();
     *out = reinterpret_cast<moe_cache *>(c);
     return MOE_OK;
     MOE_GUARD_END
+}
+
+int moe_cache_create(int n_layers, int n_experts, int ways, int top_k, moe_cache **out)
+{
+    MOE_REQUIRE(n_layers >= 1, "moe_cache_create: n_layers=%d < 1", n_layers);
+    return moe_cache_create_policy(n_layers, n_experts, ways, top_k, MOE_POLICY_LRU, nullptr, out);
+}
+
+int moe_cache_geometry(size_t budget_bytes, size_t expert_bytes, int ways, int n_layers, int *slots_out,
+                       int *covered_out)
+{
+    MOE_REQUIRE(expert_bytes > 0 && ways >= 1 && n_layers >= 0, "moe_cache_geometry: bad arguments");
+    const size_t S = budget_bytes / expert_bytes;
+    const size_t N = S / (size_t)ways;
+    if (slots_out) *slots_out = (int)std::min<size_t>(S, (size_t)INT32_MAX);
+    if (covered_out) *covered_out = (int)std::min<size_t>(N, (size_t)n_layers);
+    return MOE_OK;
 }
 
 void moe_cache_destroy(moe_cache *c) { delete reinterpret_cast<Cache *>(c); }

@@ -1,4 +1,4 @@
-// Host-side expert-cache slot table (one LRU set per layer).
+// Host-side expert-cache slot table (one set per covered layer; LRU, FIFO or static).
 #pragma once
 
 #include <cstdint>
@@ -8,6 +8,8 @@ namespace moe {
 
 struct Cache {
     int layers = 0, n = 0, ways = 0, top_k = 0;
+    int policy = 0;                     // MOE_POLICY_*
+    std::vector<int32_t> initial;       // [layers][ways] static content (MOE_POLICY_STATIC)
     std::vector<int32_t> slot_expert;   // [layers][ways], -1 empty
     std::vector<uint64_t> slot_used;    // [layers][ways], recency tick of the slot
     std::vector<uint64_t> tick;         // [layers]
@@ -17,7 +19,7 @@ struct Cache {
     void reset();
     // Step 1: slot and hit flag of each selected expert (state unchanged).
     void check(int layer, const int32_t *experts, int k, int32_t *slot_out, uint8_t *hit_out) const;
-    // LRU update for one token; outputs aligned with `experts` (nullable).
+    // Policy update for one token; outputs aligned with `experts` (nullable).
     void step(int layer, const int32_t *experts, int k, int32_t *fill_out, int32_t *evicted_out);
 };
 

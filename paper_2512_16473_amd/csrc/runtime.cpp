@@ -1,4 +1,5 @@
-// One MoE layer of single-request decode, Section III-A of the paper:
+// One MoE layer of single-request decode, Section III-A of the paper (layers past the
+// cache's covered ones, Section III-B, run every selected expert on the host):
 //   step 1  cache check of the selected experts in the layer's set;
 //   step 2a cache hits computed on the GPU from their cache slots;
 //   step 2b the hidden state copied to the host, missed experts computed there;
@@ -21,6 +22,7 @@
 // does not depend on timing.
 #include <immintrin.h>
 
+#include <algorithm>
 #include <chrono>
 #include <cstring>
 #include <vector>
@@ -155,15 +157,16 @@ int moe_runtime_create(const moe_layer_desc *desc, moe_runtime **out)
     MOE_REQUIRE(D.k >= 1 && D.k <= MOE_MAX_TOPK && D.k <= D.ways && D.ways <= D.n,
                 "moe_runtime_create: need 1 <= k <= ways <= n (k=%d ways=%d n=%d)", D.k, D.ways, D.n);
     MOE_REQUIRE(D.n_layers >= 1, "moe_runtime_create: n_layers=%d < 1", D.n_layers);
-    MOE_REQUIRE(D.w_router && D.slot_pool && D.host_slabs && D.cache && D.pool, "moe_runtime_create: null pointer");
+    MOE_REQUIRE(D.w_router && D.host_slabs && D.cache && D.pool, "moe_runtime_create: null pointer");
     MOE_REQUIRE(D.f_shared == 0 || D.shared_pool, "moe_runtime_create: f_shared > 0 needs shared_pool");
-    MOE_REQUIRE(moe::aligned16(D.w_router) && moe::aligned16(D.slot_pool) &&
+    MOE_REQUIRE(moe::aligned16(D.w_router) && (!D.slot_pool || moe::aligned16(D.slot_pool)) &&
                     (!D.shared_pool || moe::aligned16(D.shared_pool)),
                 "moe_runtime_create: device pointers must be 16-byte aligned");
     const moe::Cache *c = reinterpret_cast<const moe::Cache *>(D.cache);
-    MOE_REQUIRE(c->layers == D.n_layers && c->n == D.n && c->ways == D.ways && c->top_k == D.k,
-                "moe_runtime_create: cache geometry (L=%d n=%d ways=%d k=%d) differs from the descriptor",
+    MOE_REQUIRE(c->layers <= D.n_layers && c->n == D.n && c->ways == D.ways && c->top_k == D.k,
+                "moe_runtime_create: cache geometry (covered=%d n=%d ways=%d k=%d) does not fit the descriptor",
                 c->layers, c->n, c->ways, c->top_k);
+    MOE_REQUIRE(c->layers == 0 || D.slot_pool, "moe_runtime_create: covered layers need a slot pool");
     const size_t nh = (size_t)D.n_layers * D.n;
     for (size_t i = 0; i < nh; ++i)
         MOE_REQUIRE(D.host_slabs[i], "moe_runtime_create: host_slabs[%zu] is null", i);
@@ -206,9 +209,22 @@ int moe_runtime_create(const moe_layer_desc *desc, moe_runtime **out)
         return fail(e, "hipHostGetDevicePointer");
     if ((e = hipHostMalloc((void **)&rt->h_slotmap, sizeof(int32_t) * nh, 0)) != hipSuccess)
         return fail(e, "hipHostMalloc");
-    // Mirror of the host table as it stands now.
-    for (int l = 0; l < D.n_layers; ++l)
-        std::memcpy(rt->h_slotmap + (size_t)l * D.n, &c->where[(size_t)l * D.n], sizeof(int32_t) * D.n);
+    // Slots the cache holds already (static content, warm cache) get their slabs now.
+    for (int l = 0; l < c->layers; ++l)
+        for (int sl = 0; sl < D.ways; ++sl) {
+            const int32_t ex = c->slot_expert[(size_t)l * D.ways + sl];
+            if (ex < 0) continue;
+            uint8_t *dst = static_cast<uint8_t *>(D.slot_pool) + ((size_t)l * D.ways + sl) * rt->slab_bytes;
+            if ((e = hipMemcpy(dst, D.host_slabs[(size_t)l * D.n + ex], rt->slab_payload, hipMemcpyHostToDevice)) !=
+                hipSuccess)
+                return fail(e, "hipMemcpy(initial slot)");
+        }
+    // Mirror of the host table as it stands now; uncovered layers map nothing.
+    for (int l = 0; l < D.n_layers; ++l) {
+        int32_t *row = rt->h_slotmap + (size_t)l * D.n;
+        if (l < c->layers) std::memcpy(row, &c->where[(size_t)l * D.n], sizeof(int32_t) * D.n);
+        else std::fill(row, row + D.n, -1);
+    }
     if ((e = hipMemcpy(rt->d_slotmap, rt->h_slotmap, sizeof(int32_t) * nh, hipMemcpyHostToDevice)) != hipSuccess)
         return fail(e, "hipMemcpy(slotmap)");
     if ((e = hipEventCreateWithFlags(&rt->ev_hits, hipEventDisableTiming)) != hipSuccess) return fail(e, "event");
@@ -262,7 +278,10 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
     // Hit experts on the device (slots from the device mirror of the table).
     moe::FfnParams p{};
     p.x = x_dev;
-    p.pool = static_cast<const uint8_t *>(D.slot_pool) + (size_t)layer * D.ways * rt->slab_bytes;
+    const bool covered = layer < rt->cache->layers;
+    // An uncovered layer's mirror row is all -1, so the hit kernels take no slot from it.
+    p.pool = covered ? static_cast<const uint8_t *>(D.slot_pool) + (size_t)layer * D.ways * rt->slab_bytes
+                     : static_cast<const uint8_t *>(D.slot_pool);
     p.slab_stride = rt->slab_bytes;
     p.sel = rt->d_idx;
     p.slotmap = rt->d_slotmap + (size_t)layer * n;
@@ -306,8 +325,17 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
     std::memcpy(sel, rt->mbox->idx, sizeof(int32_t) * k);
     std::memcpy(wsel, rt->mbox->w, sizeof(float) * k);
     MOE_REQUIRE(rt->cache->valid_selection(sel, k), "moe_layer_forward: router returned an invalid selection");
-    rt->cache->check(layer, sel, k, nullptr, hit);
-    rt->cache->step(layer, sel, k, fill, evicted);
+    if (covered) {
+        rt->cache->check(layer, sel, k, nullptr, hit);
+        rt->cache->step(layer, sel, k, fill, evicted);
+    } else {   // no cache set: every expert on the host, nothing fetched
+        for (int j = 0; j < k; ++j) {
+            hit[j] = 0;
+            fill[j] = evicted[j] = -1;
+        }
+    }
+    int nfill = 0;
+    for (int j = 0; j < k; ++j) nfill += fill[j] >= 0;
 
     int nmiss = 0, nhit = 0;
     const void *mslab[MOE_MAX_TOPK];
@@ -331,10 +359,10 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
     // Step 3 starts first: post-fetch of the missed experts into their victim slots.
     // The slabs can land at once: no current-token expert is ever a victim, and the
     // previous token's kernels on this layer finished before this token's router.
-    if (nmiss) {
+    if (nfill) {
         uint8_t *set_base = static_cast<uint8_t *>(D.slot_pool) + (size_t)layer * D.ways * rt->slab_bytes;
         for (int j = 0; j < k; ++j) {
-            if (hit[j]) continue;
+            if (fill[j] < 0) continue;
             MOE_HIP(hipMemcpyAsync(set_base + (size_t)fill[j] * rt->slab_bytes,
                                    rt->host_slabs[(size_t)layer * n + sel[j]], rt->slab_payload,
                                    hipMemcpyHostToDevice, sw));
@@ -352,7 +380,7 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
     MOE_HIP(moe::launch_ffn_reduce(p, nmiss ? rt->h_y_dev + (size_t)layer * d : nullptr, out_dev, sc));
 
     // The mirror row is rewritten after this token's hit kernels have read it.
-    if (nmiss) {
+    if (nfill) {
         int32_t *row = rt->h_slotmap + (size_t)layer * n;
         std::memcpy(row, &rt->cache->where[(size_t)layer * n], sizeof(int32_t) * n);
         MOE_HIP(hipEventRecord(rt->ev_hits, sc));

@@ -68,7 +68,7 @@ WORKLOADS = {
 }
 
 # Tensor kinds used when deriving per-tensor seeds.
-_KIND = {"router": 1, "expert": 2, "shared": 3, "states": 4, "prompt": 5}
+_KIND = {"router": 1, "expert": 2, "shared": 3, "states": 4, "prompt": 5, "static-content": 6, "subsets": 7}
 _WL_ID = {name: i + 1 for i, name in enumerate(WORKLOADS)}
 
 

@@ -2,6 +2,7 @@
 host-side parts of the path (LRU slot table, host expert path) against the oracle."""
 import ctypes
 import itertools
+import json
 import random
 import re
 import os
@@ -62,7 +63,10 @@ def test_cache_create_validation():
     with pytest.raises(moe.MoeError):
         moe.Cache(2, 8, 9, 2)          # ways > n
     with pytest.raises(moe.MoeError):
-        moe.Cache(0, 8, 4, 2)
+        moe.Cache(-1, 8, 4, 2)
+    empty = moe.Cache(0, 8, 4, 2)      # no covered layer: a runtime runs every layer on the host
+    with pytest.raises(moe.MoeError):
+        empty.update(0, [1, 2])
     c = moe.Cache(2, 8, 4, 2)
     with pytest.raises(moe.MoeError):
         c.update(0, [1, 1])            # duplicate ids
@@ -123,6 +127,59 @@ def test_library_lru_long_traces_vs_oracle(n, k, ways):
             r = ref.access(layer, sel)
             assert (list(slots), list(hits), list(fill), list(ev)) == r
             assert list(c.slotmap(layer)) == ref.slotmap(layer, n)
+
+
+@pytest.mark.parametrize("policy", ["lru", "fifo", "static"])
+@pytest.mark.parametrize("n,k,ways", [(8, 2, 4), (16, 2, 6), (64, 8, 24), (4, 1, 2)])
+def test_library_policies_vs_oracle(policy, n, k, ways):
+    """Section IV-D's policies: the library's slots, hits, fills and evictions equal the
+    oracle's on correlated multi-layer traces, and reset restores the initial state."""
+    rng = random.Random(sum(map(ord, policy)) * 1000 + n * 100 + k * 10 + ways)
+    L = 3
+    content = [rng.sample(range(n), ways) for _ in range(L)] if policy == "static" else None
+    c = moe.Cache(L, n, ways, k, policy=policy, static_content=content)
+    for rep in range(2):
+        ref = olru.LRUCache(L, ways, policy=policy, static_content=content)
+        prev = [rng.sample(range(n), k) for _ in range(L)]
+        for t in range(300):
+            for layer in range(L):
+                keep = [e for e in prev[layer] if rng.random() < 0.6]
+                fresh = [e for e in rng.sample(range(n), n) if e not in keep][: k - len(keep)]
+                sel = keep + fresh
+                rng.shuffle(sel)
+                prev[layer] = sel
+                slots, hits = c.lookup(layer, sel)
+                fill, ev = c.update(layer, sel)
+                assert (list(slots), list(hits), list(fill), list(ev)) == ref.access(layer, sel)
+                assert list(c.slotmap(layer)) == ref.slotmap(layer, n)
+        c.reset()
+
+
+def test_static_policy_validation():
+    with pytest.raises(moe.MoeError):
+        moe.Cache(1, 8, 2, 2, policy="static", static_content=[[1, 1]])      # duplicate
+    with pytest.raises(moe.MoeError):
+        moe.Cache(1, 8, 2, 2, policy="static", static_content=[[1, 8]])      # out of range
+    lib = _abi.load()
+    h = ctypes.c_void_p()
+    assert lib.moe_cache_create_policy(1, 8, 2, 2, 2, None, ctypes.byref(h)) == _abi.MOE_EINVAL  # no content
+    assert lib.moe_cache_create_policy(1, 8, 2, 2, 7, None, ctypes.byref(h)) == _abi.MOE_EINVAL  # no such policy
+    # a static set may have fewer ways than top_k: misses are never inserted
+    c = moe.Cache(1, 8, 1, 2, policy="static", static_content=[[5]])
+    fill, ev = c.update(0, [5, 2])
+    assert list(fill) == [-1, -1] and list(ev) == [-1, -1]
+    assert list(c.lookup(0, [2, 5])[1]) == [False, True]
+
+
+def test_cache_geometry_vs_oracle(golden_dir):
+    """Section III-B sizing through the library equals the oracle's (and the paper's
+    worked example: 56 slots, 4 ways -> 14 indexes, layers 0-13)."""
+    ex = json.load(open(os.path.join(golden_dir, "paper_cache_sizing.json")))["example"]
+    assert moe.cache_geometry(ex["slots"], 1, ex["ways"], 32) == (ex["slots"], ex["indexes"])
+    for budget, eb, ways, L in [(24 * 10**9, 352_321_536, 4, 32), (10**12, 352_321_536, 4, 32),
+                                (3 * 10**8, 352_321_536, 4, 32), (80 * 10**9, 157_286_400, 6, 32)]:
+        S, N, covered = olru.cache_geometry(budget, eb, ways, L)
+        assert moe.cache_geometry(budget, eb, ways, L) == (S, len(covered))
 
 
 def _pool_case(d, f, ne, seed):

@@ -19,7 +19,7 @@ class World:
     """A decode world on the GPU: router weights, slot pool, pinned host experts,
     shared experts, AR(1) hidden states, library runtime."""
 
-    def __init__(self, name, L=None, T=None, ways=None, threads=4, seed=0):
+    def __init__(self, name, L=None, T=None, ways=None, threads=4, seed=0, policy="lru", covered=None):
         torch = torch_cuda()
         import paper_2512_16473_amd as moe
         wl = synth.WORKLOADS[name]
@@ -35,7 +35,13 @@ class World:
                            for l in range(self.L)])                       # [L, T, d]
         self.host, stride, self.views = make_slabs_host(torch, self.L, n, d, f, wl.w_std, seed, name)
         self.host_addrs = [self.host.ptr + i * stride for i in range(self.L * n)]
-        self.pool = torch.zeros(self.L * self.ways * stride, dtype=torch.uint8, device="cuda")
+        self.policy = policy
+        self.covered = self.L if covered is None else covered
+        # the static policy's content: a seeded uniform draw of `ways` experts per layer
+        rng = np.random.default_rng(synth.seed_for(seed, name, "static-content"))
+        self.content = [sorted(rng.choice(n, self.ways, replace=False).tolist()) for _ in range(self.covered)]
+        self.pool = (torch.zeros(self.covered * self.ways * stride, dtype=torch.uint8, device="cuda")
+                     if self.covered else None)
         self.shared = None
         self.shared_views = None
         if wl.f_shared:
@@ -43,7 +49,8 @@ class World:
                                                                   name, kind="shared")
             self.shared = torch.from_numpy(sh_host.array).cuda()
             self._sh_host = sh_host
-        self.cache = moe.Cache(self.L, n, self.ways, k)
+        self.cache = moe.Cache(self.covered, n, self.ways, k, policy=policy,
+                               static_content=self.content if policy == "static" else None)
         self.hpool = moe.HostPool(threads)
         self.rt = moe.Runtime(d, f, n, k, self.ways, self.L, torch.from_numpy(self.wr).cuda(), self.pool,
                               self.host_addrs, self.cache, self.hpool, f_shared=wl.f_shared,
@@ -72,20 +79,28 @@ class World:
 
 
 def _check_trace(world, idx, w, hit, out, steps, layers, check_out):
-    ref = olru.LRUCache(world.L, world.ways)
+    """Replays the GPU's chosen sets through the oracle's cache (same policy; layers
+    past the covered ones never hit and hold nothing)."""
+    ref = olru.LRUCache(world.covered, world.ways, policy=world.policy,
+                        static_content=world.content if world.policy == "static" else None)
     worst = 0.0
     for t in range(steps):
         for l in range(world.L):
             if l in layers:
                 oidx, ow = router_parity(idx[t, l], w[t, l], world.X[l, t], world.wr[l], world.k)
-            slots, hits, fills, ev = ref.access(l, list(idx[t, l]))
+            if l < world.covered:
+                slots, hits, fills, ev = ref.access(l, list(idx[t, l]))
+            else:
+                hits = [False] * world.k
             assert list(hit[t, l]) == hits, (t, l, list(hit[t, l]), hits)
             if l in layers and check_out(t, l):
                 o = world.oracle_out(l, t, oidx)
                 worst = max(worst, assert_close(out[t, l], o, f"t={t} layer={l}"))
     for l in range(world.L):
-        assert list(world.rt.device_slotmap(l)) == ref.slotmap(l, world.n)
-        assert list(world.cache.slotmap(l)) == ref.slotmap(l, world.n)
+        expect = ref.slotmap(l, world.n) if l < world.covered else [-1] * world.n
+        assert list(world.rt.device_slotmap(l)) == expect
+        if l < world.covered:
+            assert list(world.cache.slotmap(l)) == expect
     return worst
 
 
@@ -126,4 +141,46 @@ def test_runtime_full_shapes(name, L, T, layers):
     world = World(name, L=L, T=T, threads=8)
     idx, w, hit, out = world.run(T)
     worst = _check_trace(world, idx, w, hit, out, T, layers, lambda t, l: t % 3 == 0 or t == T - 1)
+    say("  worst max|err|/RMS", worst)
+
+
+@pytest.mark.parametrize("policy", ["fifo", "static"])
+def test_runtime_tiny_policies(policy):
+    """Section IV-D's other policies through the whole path: FIFO (post-fetch as LRU,
+    no refresh on hits) and static (fixed content loaded at creation, misses never
+    fetched). Trace bit-exact against the oracle's policy, outputs within tolerance."""
+    say("runtime tiny policy", policy)
+    world = World("tiny", policy=policy)
+    steps = world.T
+    idx, w, hit, out = world.run(steps)
+    worst = _check_trace(world, idx, w, hit, out, steps, set(range(world.L)), lambda t, l: True)
+    st = world.rt.stats()
+    assert st["expert_hits"] + st["expert_misses"] == steps * world.L * world.k
+    assert st["fills"] == (0 if policy == "static" else st["expert_misses"])
+    say("  worst max|err|/RMS", worst, "hit rate", st["expert_hits"] / (steps * world.k))
+
+
+@pytest.mark.parametrize("covered", [0, 1, 2])
+def test_runtime_uncovered_layers(covered):
+    """Section III-B: a memory budget covers layers 0..N-1 only; the other layers run
+    every selected expert on the host and fetch nothing. Three tiny-shaped layers."""
+    say("runtime tiny, 3 layers, covered", covered)
+    world = World("tiny", L=3, T=20, covered=covered)
+    idx, w, hit, out = world.run(20)
+    worst = _check_trace(world, idx, w, hit, out, 20, {0, 1, 2}, lambda t, l: True)
+    st = world.rt.stats()
+    assert not hit[:, covered:].any()
+    assert st["fills"] == st["expert_misses"] - 20 * (3 - covered) * world.k
+    say("  worst max|err|/RMS", worst)
+
+
+def test_runtime_mixtral_static_policy():
+    """Mixtral-shaped layer with a static 4-of-8 content: the four resident slabs are
+    loaded at creation and every other expert always runs on the host."""
+    oracle.set_threads(min(16, os.cpu_count() or 1))
+    say("runtime mixtral static")
+    world = World("mixtral", L=1, T=6, threads=8, policy="static")
+    idx, w, hit, out = world.run(6)
+    worst = _check_trace(world, idx, w, hit, out, 6, {0}, lambda t, l: True)
+    assert world.rt.stats()["fills"] == 0
     say("  worst max|err|/RMS", worst)

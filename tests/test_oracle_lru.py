@@ -96,16 +96,25 @@ def test_slot_assignment_trace():
     assert s.access([0, 2]) == ([0, 1], [True, True], [-1, -1], [-1, -1])
 
 
-def test_random_policy_closed_form(golden_dir):
-    """Section IV-D: with i.i.d. uniform expert pairs the cache content is independent
-    of the next draw, so LRU's long-run hit rates equal the static-random formulas."""
+def _make_set(policy, n, M, rng):
+    if policy == "static":
+        return lru.StaticSet(M, rng.sample(range(n), M))
+    return {"lru": lru.LRUSet, "fifo": lru.FIFOSet}[policy](M)
+
+
+@pytest.mark.parametrize("policy", ["lru", "fifo", "static"])
+def test_random_policy_closed_form(golden_dir, policy):
+    """Section IV-D: a static random set of M experts hits with the closed-form
+    probabilities. With i.i.d. uniform expert pairs the content of an LRU or FIFO
+    cache is independent of the next draw too, so their long-run hit rates must
+    converge to the same formulas."""
     data = json.load(open(os.path.join(golden_dir, "paper_random_policy.json")))
     for c in data["cases"]:
         n, M = c["n"], c["M"]
         p_any = 1 - ((n - M) / n) * ((n - M - 1) / (n - 1))
         p_both = (M / n) * ((M - 1) / (n - 1))
         rng = random.Random(n * 31 + M)
-        s = lru.LRUSet(M)
+        s = _make_set(policy, n, M, rng)
         N = 20000
         any_hits = both_hits = 0
         for t in range(N + 50):
@@ -136,3 +145,76 @@ def test_rejects_bad_access():
         s.access([1, 1])
     with pytest.raises(ValueError):
         s.access([0, 1, 2])
+
+
+# ---- FIFO and static (Section IV-D's comparison policies) ---------------------------
+
+@pytest.mark.parametrize("ways", [1, 2, 3, 4])
+def test_fifo_k1_exhaustive_vs_textbook(ways):
+    """k = 1: the procedural FIFO set equals a plain bounded queue on every
+    sequence of length 6 over 4 experts."""
+    for seq in itertools.product(range(4), repeat=6):
+        s = lru.FIFOSet(ways)
+        hits = [s.access([e])[1][0] for e in seq]
+        assert hits == lru.textbook_fifo_hits(list(seq), ways), seq
+
+
+def test_fifo_differs_from_lru_by_hand():
+    """M = 2, k = 1, accesses 1 2 1 3 1: LRU keeps 1 (refreshed by its hit) and evicts
+    2; FIFO evicts 1, the earliest inserted, so the last access misses."""
+    seq = [1, 2, 1, 3, 1]
+    lru_s, fifo_s = lru.LRUSet(2), lru.FIFOSet(2)
+    assert [lru_s.access([e])[1][0] for e in seq] == [False, False, True, False, True]
+    assert [fifo_s.access([e])[1][0] for e in seq] == [False, False, True, False, False]
+
+
+@pytest.mark.parametrize("n,k,ways", [(8, 2, 4), (16, 2, 6), (64, 8, 24), (4, 2, 2)])
+def test_fifo_invariants(n, k, ways):
+    """Capacity, no duplicates, every selected expert cached after its token, a
+    current expert never evicted, and a hit never changes any slot or stamp."""
+    rng = random.Random(7 * n + k + ways)
+    s = lru.FIFOSet(ways)
+    prev_content = set()
+    for _ in range(400):
+        sel = rng.sample(range(n), k)
+        before = (list(s.expert), list(s.stamp))
+        slots, hits, fills, evicted = s.access(sel)
+        for j, e in enumerate(sel):
+            assert hits[j] == (e in prev_content)
+            if not hits[j]:
+                assert evicted[j] not in sel
+        if all(hits):
+            assert (list(s.expert), list(s.stamp)) == before
+        occupied = [e for e in s.expert if e >= 0]
+        assert len(occupied) == len(set(occupied)) <= ways
+        assert set(sel) <= s.content()
+        prev_content = s.content()
+
+
+def test_fifo_evicts_in_insertion_order():
+    """With every slot full and no current-token conflicts, the victims come out in
+    the order the experts went in, whatever the hits in between."""
+    s = lru.FIFOSet(3)
+    for e in (5, 6, 7):
+        s.access([e])
+    s.access([5])          # a hit: FIFO does not refresh
+    s.access([6])
+    _, _, _, ev = s.access([8])
+    assert ev == [5]
+    _, _, _, ev = s.access([9])
+    assert ev == [6]
+
+
+def test_static_set_never_changes():
+    rng = random.Random(3)
+    content = [4, 1, 6, 2]
+    s = lru.StaticSet(4, content)
+    for _ in range(200):
+        sel = rng.sample(range(8), 2)
+        slots, hits, fills, evicted = s.access(sel)
+        assert hits == [e in content for e in sel]
+        assert slots == [content.index(e) if e in content else -1 for e in sel]
+        assert fills == [-1, -1] and evicted == [-1, -1]
+        assert s.expert == content
+    with pytest.raises(ValueError):
+        lru.StaticSet(2, [1, 1])
