@@ -56,6 +56,15 @@ def build_world(torch, moe, synth, wl, steps_total, seed, threads, pinned_gb, po
             hview[e * stride: e * stride + 3 * d * f * 2].copy_(tmp.view(torch.uint8))
     del tmp
     log(f"expert weights drawn: {time.perf_counter() - t0:.1f}s")
+    # The weights reached the pinned pages by DMA, so the CPU has never touched them; on
+    # these hosts the first CPU access to each page is ~1 us (13x the steady-state FFN
+    # time). Weights loaded from disk by the CPU would be touched already, so touch
+    # every page once here, outside any timed region, from all host threads.
+    from concurrent.futures import ThreadPoolExecutor
+    chunks = [(hh, o) for hh in range(H) for o in range(0, per_layer, 1 << 28)]
+    with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+        list(ex.map(lambda c: int(hosts[c[0]].array[c[1]:c[1] + (1 << 28):4096].sum()), chunks))
+    log(f"host pages touched: {time.perf_counter() - t0:.1f}s")
     host_addrs = [hosts[l % H].ptr + e * stride for l in range(L) for e in range(n)]
     shared = None
     if wl.f_shared:
@@ -79,11 +88,17 @@ def build_world(torch, moe, synth, wl, steps_total, seed, threads, pinned_gb, po
     cache = moe.Cache(covered, n, M, k, policy=policy, static_content=content)
     hp = moe.HostPool(threads)
     rt = moe.Runtime(d, f, n, k, M, L, wr, pool, host_addrs, cache, hp, f_shared=wl.f_shared, shared_pool=shared)
+
+    def fresh_runtime():
+        """A new cold cache and runtime over the same weights (for a second measurement)."""
+        c2 = moe.Cache(covered, n, M, k, policy=policy, static_content=content)
+        return c2, moe.Runtime(d, f, n, k, M, L, wr, pool, host_addrs, c2, hp, f_shared=wl.f_shared,
+                               shared_pool=shared)
     torch.cuda.synchronize()
     log(f"world ready in {time.perf_counter() - t0:.1f}s (device cache {0 if pool is None else pool.numel() / 1e9:.1f} GB, "
         f"{covered} of {L} layers covered, policy {policy})")
     return dict(hosts=hosts, H=H, wr=wr, X=X, xd=xd, pool=pool, shared=shared, cache=cache, hp=hp, rt=rt,
-                stride=stride, covered=covered, policy=policy)
+                stride=stride, covered=covered, policy=policy, fresh_runtime=fresh_runtime)
 
 
 def cpu_baseline(wl, world, seed, budget_s, t_first):
@@ -213,6 +228,55 @@ def hit_study(args, torch, moe, synth, wl):
     }
 
 
+def pcie_study(args, torch, moe, synth, wl):
+    """Host-to-device expert copies (the transfer column of the paper's Table I and
+    Table III): one expert slab from pinned memory on one stream, two slabs on two
+    streams at once (two DMA engines, Section III-C), and one slab from pageable memory."""
+    import numpy as np
+    stride = moe.slab_bytes(wl.d, wl.f)
+    payload = 3 * wl.d * wl.f * 2
+    src = [torch.ones(payload, dtype=torch.uint8, pin_memory=True) for _ in range(2)]   # hipHostMalloc'd
+    pageable = torch.ones(payload, dtype=torch.uint8)
+    dst = torch.empty(2 * stride, dtype=torch.uint8, device="cuda")
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+
+    def timed(fn, reps=5):
+        ts = []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            fn()
+            torch.cuda.synchronize()
+            ts.append(time.perf_counter() - t0)
+        return sorted(ts)[len(ts) // 2]
+
+    def one():
+        with torch.cuda.stream(s1):
+            dst[:payload].copy_(src[0], non_blocking=True)
+
+    def two():
+        with torch.cuda.stream(s1):
+            dst[:payload].copy_(src[0], non_blocking=True)
+        with torch.cuda.stream(s2):
+            dst[stride:stride + payload].copy_(src[1], non_blocking=True)
+
+    def page():
+        dst[:payload].copy_(pageable)
+
+    t1, t2, tp = timed(one), timed(two), timed(page, reps=3)
+    res = {
+        "metric": "host-to-device expert copy bandwidth (pinned, 1 and 2 streams; pageable)",
+        "value": round(payload / t1 / 1e9, 2), "unit": "GB/s (one pinned slab, one stream)",
+        "n_gpus": 1, "higher_is_better": True, "data": "synthetic",
+        "config": {"workload": wl.desc, "slab_bytes": payload},
+        "one_stream": {"ms": round(t1 * 1e3, 2), "GB/s": round(payload / t1 / 1e9, 2)},
+        "two_streams": {"ms": round(t2 * 1e3, 2), "GB/s": round(2 * payload / t2 / 1e9, 2)},
+        "pageable": {"ms": round(tp * 1e3, 2), "GB/s": round(payload / tp / 1e9, 2)},
+    }
+    log(json.dumps(res))
+    return res
+
+
 def measured_traffic(args):
     """HBM bytes per k_gate_up launch from the committed PMC record, if it was taken on
     the current kernel source and the same workload arguments; else None."""
@@ -310,8 +374,11 @@ def main():
                     help="cache replacement policy (Section IV-D; the paper's is LRU)")
     ap.add_argument("--budget-gb", type=float, default=None,
                     help="GPU memory for the expert cache (GB); layers past the covered ones run on the host")
+    ap.add_argument("--fill-limit", type=int, default=0,
+                    help="bounded post-fetch: at most this many expert slabs in flight (0: every miss fetched)")
     ap.add_argument("--hit-study", action="store_true",
                     help="only replay router selections through LRU/FIFO/static caches of several sizes")
+    ap.add_argument("--pcie", action="store_true", help="only measure host-to-device expert copies")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB 5 times (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -337,6 +404,9 @@ def main():
         print(json.dumps({"copy_calibration_bytes_read": nbytes, "copy_calibration_bytes_written": nbytes}))
         return
     wl = synth.WORKLOADS[args.workload]
+    if args.pcie:
+        print(json.dumps(pcie_study(args, torch, moe, synth, wl)), flush=True)
+        return
     if args.hit_study:
         print(json.dumps(hit_study(args, torch, moe, synth, wl)), flush=True)
         return
@@ -348,6 +418,7 @@ def main():
     world = build_world(torch, moe, synth, wl, steps_total, args.seed, args.threads, args.pinned_gb,
                         policy=args.policy, budget_gb=args.budget_gb)
     rt, xd = world["rt"], world["xd"]
+    rt.set_fill_limit(args.fill_limit)
     L, k, d = wl.L, wl.k, wl.d
     out = torch.empty((2, L, d), dtype=torch.float32, device="cuda")
     streams = (torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream())
@@ -401,6 +472,8 @@ def main():
             "host_threads": world["hp"].threads, "parallelism": "single GPU",
             "host_expert_layers_distinct": world["H"],
             "cache_policy": world["policy"], "covered_layers": world["covered"],
+            "post_fetch": (f"at most {args.fill_limit} slabs in flight" if args.fill_limit
+                           else "every miss (Section III-A step 3)"),
         },
         "roofline": {
             "kernel": "k_gate_up (W1/W3 rows + SiLU*mul)",
@@ -428,6 +501,7 @@ def main():
             "host_ffn_ms_per_token": round(st["host_ffn_ms"] / K, 3),
             "route_wait_ms_per_token": round(st["route_wait_ms"] / K, 3),
             "fills_per_token": round(st["fills"] / K, 3),
+            "fills_skipped_per_token": round(st["fills_skipped"] / K, 3),
         },
     }
     log(json.dumps(result["trace"]), json.dumps(result["hit_ffn"]))
@@ -435,6 +509,33 @@ def main():
         "what": f"host FFN of one layer's {k} experts (all missed), alone, by thread count",
         "by_threads": host_sweep(moe, wl, world)}
     log(json.dumps(result["host_expert_layer"]))
+    if args.fill_limit == 0 and world["policy"] != "static" and world["covered"] > 0:
+        # The same tokens once more, cold cache, with bounded post-fetch (at most two
+        # slabs in flight): misses beyond that run on the host without being fetched.
+        rt.close()
+        world["cache"], rt2 = world["fresh_runtime"]()
+        rt2.set_fill_limit(2)
+        for t in range(args.warmup):
+            rt2.decode_step(xd[t], out[t % 2], streams, idx, wts, hit)
+        torch.cuda.synchronize()
+        rt2.sync()
+        rt2.reset_stats()
+        t0 = time.perf_counter()
+        for t in range(args.warmup, steps_total):
+            rt2.decode_step(xd[t], out[t % 2], streams, idx, wts, hit)
+        torch.cuda.synchronize()
+        rt2.sync()
+        dt2 = time.perf_counter() - t0
+        s2 = rt2.stats()
+        result["bounded_post_fetch"] = {
+            "what": "same timed tokens, cold cache, at most 2 expert slabs in flight (misses beyond run on the host, "
+                    "not fetched)",
+            "tokens_per_s": round(K / dt2, 3), "ms_per_step": round(dt2 / K * 1e3, 3),
+            "expert_hit_rate": round(s2["expert_hits"] / max(1, s2["expert_hits"] + s2["expert_misses"]), 4),
+            "fills_per_token": round(s2["fills"] / K, 3), "fills_skipped_per_token": round(s2["fills_skipped"] / K, 3),
+            "host_ffn_ms_per_token": round(s2["host_ffn_ms"] / K, 3)}
+        log(json.dumps(result["bounded_post_fetch"]))
+        rt = rt2
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, world, args.seed, args.cpu_baseline_s, args.warmup)
     else:

@@ -137,6 +137,14 @@ int moe_cache_lookup(const moe_cache *c, int layer, const int32_t *experts, int 
  */
 int moe_cache_update(moe_cache *c, int layer, const int32_t *experts, int k,
                      int32_t *fill_slot_out, int32_t *evicted_out);
+/*
+ * moe_cache_update where insert (host uint8 [k], aligned with `experts`, NULL = all 1)
+ * marks which misses may be inserted: a miss with insert[j] = 0 (its post-fetch was not
+ * issued) takes no slot and evicts nothing (fill_slot_out[j] = evicted_out[j] = -1),
+ * though it still advances the set's clock. Hits ignore the mask.
+ */
+int moe_cache_update_masked(moe_cache *c, int layer, const int32_t *experts, int k,
+                            const uint8_t *insert, int32_t *fill_slot_out, int32_t *evicted_out);
 /* Expert -> slot table of one layer: host [n], -1 for experts not cached. */
 int moe_cache_slotmap(const moe_cache *c, int layer, int32_t *slotmap_out);
 
@@ -255,6 +263,17 @@ int moe_decode_step(moe_runtime *rt, const float *x_dev, float *out_dev, int32_t
                     float *w_host, uint8_t *hit_host, void *compute_stream, void *act_stream,
                     void *copy_stream);
 
+/*
+ * Bounded post-fetch. With max_slabs_in_flight = Q > 0, a missed expert is post-fetched
+ * (and inserted into the cache) only while fewer than Q slabs are still being copied on
+ * the copy stream; the other misses run on the host as usual but are not inserted
+ * (moe_cache_update_masked semantics), so tokens never queue behind a backlog of
+ * weight copies. The budget goes to the misses in ascending expert id. Which misses are
+ * inserted then depends on copy timing; the cache table records it. Q = 0 (the
+ * default) inserts every miss, as Section III-A step 3 describes.
+ */
+int moe_runtime_set_fill_limit(moe_runtime *rt, int max_slabs_in_flight);
+
 /* Blocks until every copy the runtime enqueued has finished. */
 int moe_runtime_sync(moe_runtime *rt);
 
@@ -276,6 +295,7 @@ typedef struct moe_runtime_stats {
     int64_t down_launches;
     double down_ms;
     double down_bytes;
+    int64_t fills_skipped;    /* misses not post-fetched because of the fill limit */
 } moe_runtime_stats;
 
 /*

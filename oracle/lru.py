@@ -52,16 +52,21 @@ class LRUSet:
         slots = [self.expert.index(e) if e in self.expert else -1 for e in selected]
         return slots, [s >= 0 for s in slots]
 
-    def access(self, selected: Sequence[int]):
+    def access(self, selected: Sequence[int], insert=None):
         """Check, then update for one token. `selected` is in rank order.
+
+        insert (optional, aligned with `selected`): False for a missed expert that must
+        not be inserted (its post-fetch was not issued); such a miss takes no slot and
+        evicts nothing, though it still takes its clock tick.
 
         Returns (slots, hits, fills, evicted), each aligned with `selected`:
         slots[j]   slot holding expert j before the update (-1 on miss)
         hits[j]    whether expert j was cached before the token
-        fills[j]   slot expert j was inserted into (-1 on hit)
+        fills[j]   slot expert j was inserted into (-1 on hit or when not inserted)
         evicted[j] expert removed to make room for j (-1 if none)
         """
         sel = list(selected)
+        allow = dict(zip(sel, [True] * len(sel) if insert is None else [bool(v) for v in insert]))
         if len(set(sel)) != len(sel):
             raise ValueError("selected experts must be distinct")
         if len(sel) > self.ways:
@@ -74,6 +79,8 @@ class LRUSet:
             self.clock += 1
             if hit_of[e]:
                 self.stamp[self.expert.index(e)] = self.clock
+                continue
+            if not allow[e]:
                 continue
             empty = [s for s in range(self.ways) if self.expert[s] < 0]
             if empty:
@@ -94,12 +101,13 @@ class FIFOSet(LRUSet):
     """One set with first-in-first-out replacement: a hit leaves the stamps alone,
     so a slot's stamp is the clock of its insertion."""
 
-    def access(self, selected: Sequence[int]):
+    def access(self, selected: Sequence[int], insert=None):
         sel = list(selected)
         if len(set(sel)) != len(sel):
             raise ValueError("selected experts must be distinct")
         if len(sel) > self.ways:
             raise ValueError("more selected experts than ways")
+        allow = dict(zip(sel, [True] * len(sel) if insert is None else [bool(v) for v in insert]))
         slots, hits = self.lookup(sel)
         hit_of = dict(zip(sel, hits))
         current = set(sel)
@@ -108,6 +116,8 @@ class FIFOSet(LRUSet):
             self.clock += 1
             if hit_of[e]:
                 continue                      # no refresh: insertion order decides
+            if not allow[e]:
+                continue
             empty = [s for s in range(self.ways) if self.expert[s] < 0]
             if empty:
                 victim = empty[0]
@@ -133,7 +143,7 @@ class StaticSet(LRUSet):
             raise ValueError("static content must be `ways` distinct expert ids")
         self.expert = content
 
-    def access(self, selected: Sequence[int]):
+    def access(self, selected: Sequence[int], insert=None):
         sel = list(selected)
         if len(set(sel)) != len(sel):
             raise ValueError("selected experts must be distinct")
@@ -157,8 +167,8 @@ class LRUCache:
         else:
             self.sets = [POLICIES[policy](ways) for _ in range(n_layers)]
 
-    def access(self, layer: int, selected: Sequence[int]):
-        return self.sets[layer].access(selected)
+    def access(self, layer: int, selected: Sequence[int], insert=None):
+        return self.sets[layer].access(selected, insert)
 
     def slotmap(self, layer: int, n_experts: int) -> List[int]:
         """Expert -> slot table of one layer (-1 when not cached)."""
@@ -186,6 +196,27 @@ def definitional_hits(trace: Iterable[Sequence[int]], ways: int) -> List[List[bo
             key[e] = (t, pos)
         ranked = sorted(key, key=lambda e: key[e], reverse=True)
         content = set(ranked[:ways])
+    return out
+
+
+def definitional_hits_masked(trace: Iterable[Sequence[int]], inserts: Iterable[Sequence[bool]],
+                             ways: int) -> List[List[bool]]:
+    """`definitional_hits` when some misses are not inserted: the content after token t
+    is the min(M, size) experts with the largest keys among the content after token
+    t-1 plus the misses of token t that were inserted; hits and inserted misses take
+    the key (t, position in ascending-id order)."""
+    key = {}
+    content: set = set()
+    out = []
+    for t, (sel, ins) in enumerate(zip(trace, inserts)):
+        hits = [e in content for e in sel]
+        out.append(hits)
+        allow = dict(zip(sel, ins))
+        for pos, e in enumerate(sorted(sel)):
+            if e in content or allow[e]:
+                key[e] = (t, pos)
+        pool = content | {e for e in sel if allow[e]}
+        content = set(sorted(pool, key=lambda e: key[e], reverse=True)[:ways])
     return out
 
 

@@ -97,7 +97,7 @@ class Cache:
         self.n_layers, self.n, self.ways, self.k, self.policy = n_layers, n_experts, ways, top_k, policy
 
     def close(self):
-        if getattr(self, "handle", None):
+        if getattr(self, "handle", None) and _lib is not None:
             _lib.moe_cache_destroy(self.handle)
             self.handle = None
 
@@ -121,6 +121,17 @@ class Cache:
         ev = np.empty(e.size, np.int32)
         _check("moe_cache_update", _lib.moe_cache_update(self.handle, layer, _np_ptr(e, ctypes.c_int32), e.size,
                                                          _np_ptr(fill, ctypes.c_int32), _np_ptr(ev, ctypes.c_int32)))
+        return fill, ev
+
+    def update_masked(self, layer, experts, insert):
+        e = np.ascontiguousarray(experts, dtype=np.int32)
+        ins = np.ascontiguousarray(insert, dtype=np.uint8)
+        fill = np.empty(e.size, np.int32)
+        ev = np.empty(e.size, np.int32)
+        _check("moe_cache_update_masked",
+               _lib.moe_cache_update_masked(self.handle, layer, _np_ptr(e, ctypes.c_int32), e.size,
+                                            _np_ptr(ins, ctypes.c_uint8), _np_ptr(fill, ctypes.c_int32),
+                                            _np_ptr(ev, ctypes.c_int32)))
         return fill, ev
 
     def slotmap(self, layer):
@@ -170,7 +181,7 @@ class PinnedBuffer:
         self.array = np.ctypeslib.as_array((ctypes.c_uint8 * self.nbytes).from_address(self.ptr))
 
     def close(self):
-        if getattr(self, "ptr", None):
+        if getattr(self, "ptr", None) and _lib is not None:
             self.array = None
             _lib.moe_host_free(ctypes.c_void_p(self.ptr))
             self.ptr = None
@@ -191,7 +202,7 @@ class HostPool:
         return int(_lib.moe_host_pool_threads(self.handle))
 
     def close(self):
-        if getattr(self, "handle", None):
+        if getattr(self, "handle", None) and _lib is not None:
             _lib.moe_host_pool_destroy(self.handle)
             self.handle = None
 
@@ -241,7 +252,7 @@ class Runtime:
         self.d, self.f, self.n, self.k, self.ways, self.L = d, f, n, k, ways, n_layers
 
     def close(self):
-        if getattr(self, "handle", None):
+        if getattr(self, "handle", None) and _lib is not None:
             _lib.moe_runtime_destroy(self.handle)
             self.handle = None
 
@@ -278,6 +289,9 @@ class Runtime:
 
     def set_timing(self, on: bool):
         _check("moe_runtime_set_timing", _lib.moe_runtime_set_timing(self.handle, 1 if on else 0))
+
+    def set_fill_limit(self, max_slabs_in_flight):
+        _check("moe_runtime_set_fill_limit", _lib.moe_runtime_set_fill_limit(self.handle, int(max_slabs_in_flight)))
 
     def stats(self) -> dict:
         s = RuntimeStats()

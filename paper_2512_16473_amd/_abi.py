@@ -35,6 +35,7 @@ class RuntimeStats(ctypes.Structure):
         ("host_ffn_ms", c_double), ("route_wait_ms", c_double),
         ("gate_up_launches", ctypes.c_int64), ("gate_up_ms", c_double), ("gate_up_bytes", c_double),
         ("down_launches", ctypes.c_int64), ("down_ms", c_double), ("down_bytes", c_double),
+        ("fills_skipped", ctypes.c_int64),
     ]
 
 
@@ -56,6 +57,7 @@ SIGNATURES = [
     ("moe_cache_reset", c_int, [c_void_p]),
     ("moe_cache_lookup", c_int, [c_void_p, c_int, c_i32p, c_int, c_i32p, c_u8p]),
     ("moe_cache_update", c_int, [c_void_p, c_int, c_i32p, c_int, c_i32p, c_i32p]),
+    ("moe_cache_update_masked", c_int, [c_void_p, c_int, c_i32p, c_int, c_u8p, c_i32p, c_i32p]),
     ("moe_cache_slotmap", c_int, [c_void_p, c_int, c_i32p]),
     ("moe_ffn_workspace_bytes", c_size_t, [c_int, c_int, c_int]),
     ("moe_expert_ffn_hits", c_int, [c_void_p, c_void_p, c_int, c_void_p, c_void_p, c_int, c_int, c_int,
@@ -76,6 +78,7 @@ SIGNATURES = [
                                 c_void_p, c_void_p, c_void_p]),
     ("moe_runtime_sync", c_int, [c_void_p]),
     ("moe_runtime_device_slotmap", c_int, [c_void_p, c_int, c_i32p]),
+    ("moe_runtime_set_fill_limit", c_int, [c_void_p, c_int]),
     ("moe_runtime_set_timing", c_int, [c_void_p, c_int]),
     ("moe_runtime_get_stats", c_int, [c_void_p, ctypes.POINTER(RuntimeStats)]),
     ("moe_runtime_reset_stats", c_int, [c_void_p]),

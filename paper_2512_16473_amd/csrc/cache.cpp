@@ -47,7 +47,8 @@ void Cache::check(int layer, const int32_t *experts, int k, int32_t *slot_out, u
     }
 }
 
-void Cache::step(int layer, const int32_t *experts, int k, int32_t *fill_out, int32_t *evicted_out)
+void Cache::step(int layer, const int32_t *experts, int k, int32_t *fill_out, int32_t *evicted_out,
+                 const uint8_t *allow)
 {
     int32_t *sx = &slot_expert[(size_t)layer * ways];
     uint64_t *su = &slot_used[(size_t)layer * ways];
@@ -76,6 +77,11 @@ void Cache::step(int layer, const int32_t *experts, int k, int32_t *fill_out, in
         ++clk;
         if (hit[j]) {
             if (policy == MOE_POLICY_LRU) su[map[e]] = clk;   // FIFO keeps the insertion stamp
+            if (fill_out) fill_out[j] = -1;
+            if (evicted_out) evicted_out[j] = -1;
+            continue;
+        }
+        if (allow && !allow[j]) {   // post-fetch not issued: the miss takes no slot
             if (fill_out) fill_out[j] = -1;
             if (evicted_out) evicted_out[j] = -1;
             continue;
@@ -202,6 +208,18 @@ int moe_cache_update(moe_cache *ch, int layer, const int32_t *experts, int k, in
     MOE_REQUIRE(c->valid_selection(experts, k),
                 "moe_cache_update: need 1 <= k <= top_k distinct expert ids in [0,%d)", c->n);
     c->step(layer, experts, k, fill_slot_out, evicted_out);
+    return MOE_OK;
+}
+
+int moe_cache_update_masked(moe_cache *ch, int layer, const int32_t *experts, int k, const uint8_t *insert,
+                            int32_t *fill_slot_out, int32_t *evicted_out)
+{
+    Cache *c = reinterpret_cast<Cache *>(ch);
+    MOE_REQUIRE(c && experts, "moe_cache_update_masked: null pointer");
+    MOE_REQUIRE(layer >= 0 && layer < c->layers, "moe_cache_update_masked: layer=%d out of [0,%d)", layer, c->layers);
+    MOE_REQUIRE(c->valid_selection(experts, k),
+                "moe_cache_update_masked: need 1 <= k <= top_k distinct expert ids in [0,%d)", c->n);
+    c->step(layer, experts, k, fill_slot_out, evicted_out, insert);
     return MOE_OK;
 }
 

@@ -20,7 +20,9 @@ struct Cache {
     // Step 1: slot and hit flag of each selected expert (state unchanged).
     void check(int layer, const int32_t *experts, int k, int32_t *slot_out, uint8_t *hit_out) const;
     // Policy update for one token; outputs aligned with `experts` (nullable).
-    void step(int layer, const int32_t *experts, int k, int32_t *fill_out, int32_t *evicted_out);
+    // allow (nullable, aligned with `experts`): 0 for a miss that must not be inserted.
+    void step(int layer, const int32_t *experts, int k, int32_t *fill_out, int32_t *evicted_out,
+              const uint8_t *allow = nullptr);
 };
 
 }  // namespace moe

@@ -24,6 +24,7 @@
 
 #include <algorithm>
 #include <chrono>
+#include <deque>
 #include <cstring>
 #include <vector>
 
@@ -65,6 +66,7 @@ struct moe_runtime {
     moe::RouteMailbox *mbox = nullptr, *mbox_dev = nullptr;
     float *h_x = nullptr, *h_x_dev = nullptr;   // [d] hidden state of the current layer call
     float *h_y = nullptr, *h_y_dev = nullptr;   // [L][d] host-path output per layer
+    std::vector<float> x_local, y_local;        // [d] cached host copies for the host FFN
     int32_t seq = 0;
     // pinned staging of the mirror rows for the copy stream
     int32_t *h_slotmap = nullptr;   // [L][n]
@@ -72,6 +74,13 @@ struct moe_runtime {
     hipEvent_t ev_hits = nullptr;
     std::vector<hipEvent_t> ev_fill;   // [L]
     std::vector<char> fill_pending;    // [L]
+
+    // Bounded post-fetch: at most fill_limit slabs queued on the copy stream (0: no
+    // bound). Fills complete in issue order (one stream), so a FIFO of per-call events
+    // tells how many slabs are still in flight.
+    int fill_limit = 0;
+    std::deque<std::pair<hipEvent_t, int>> inflight;
+    std::vector<hipEvent_t> fill_spare;
 
     bool timing = false;
     std::vector<TimingRec> pending;    // recorded, not yet resolved
@@ -88,6 +97,8 @@ void release(moe_runtime *rt)
     for (auto &r : rt->pending)
         for (auto e : r.ev) (void)hipEventDestroy(e);
     for (auto e : rt->spare) (void)hipEventDestroy(e);
+    for (auto &q : rt->inflight) (void)hipEventDestroy(q.first);
+    for (auto e : rt->fill_spare) (void)hipEventDestroy(e);
     for (auto e : rt->ev_fill)
         if (e) (void)hipEventDestroy(e);
     if (rt->ev_hits) (void)hipEventDestroy(rt->ev_hits);
@@ -132,6 +143,19 @@ int resolve_timing(moe_runtime *rt)
     }
     rt->pending.clear();
     return MOE_OK;
+}
+
+// Slabs still being copied: retire completed entries from the front of the FIFO.
+int slabs_in_flight(moe_runtime *rt)
+{
+    while (!rt->inflight.empty() && hipEventQuery(rt->inflight.front().first) == hipSuccess) {
+        rt->fill_spare.push_back(rt->inflight.front().first);
+        rt->inflight.pop_front();
+    }
+    (void)hipGetLastError();   // a not-ready query leaves hipErrorNotReady behind
+    int n = 0;
+    for (auto &q : rt->inflight) n += q.second;
+    return n;
 }
 
 double now_ms()
@@ -180,6 +204,8 @@ int moe_runtime_create(const moe_layer_desc *desc, moe_runtime **out)
     rt->shared_bytes = D.f_shared ? moe_slab_bytes(D.d, D.f_shared) : 0;
     rt->cache = reinterpret_cast<moe::Cache *>(D.cache);
     rt->pool = reinterpret_cast<moe::HostPool *>(D.pool);
+    rt->x_local.assign(D.d, 0.f);
+    rt->y_local.assign(D.d, 0.f);
 
     auto fail = [&](hipError_t e, const char *what) {
         moe::set_error("moe_runtime_create: %s failed: %s", what, hipGetErrorString(e));
@@ -327,7 +353,26 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
     MOE_REQUIRE(rt->cache->valid_selection(sel, k), "moe_layer_forward: router returned an invalid selection");
     if (covered) {
         rt->cache->check(layer, sel, k, nullptr, hit);
-        rt->cache->step(layer, sel, k, fill, evicted);
+        uint8_t allow[MOE_MAX_TOPK];
+        const uint8_t *allow_p = nullptr;
+        if (rt->fill_limit > 0) {
+            // The misses the cache would insert, in its (ascending-id) order, get the
+            // remaining copy budget; the others stay on the host and are not inserted.
+            int budget = rt->fill_limit - slabs_in_flight(rt);
+            int order[MOE_MAX_TOPK];
+            for (int j = 0; j < k; ++j) order[j] = j;
+            std::sort(order, order + k, [&](int a, int b) { return sel[a] < sel[b]; });
+            for (int q = 0; q < k; ++q) {
+                const int j = order[q];
+                allow[j] = 1;
+                if (!hit[j]) {
+                    allow[j] = budget > 0;
+                    budget -= allow[j];
+                }
+            }
+            allow_p = allow;
+        }
+        rt->cache->step(layer, sel, k, fill, evicted, allow_p);
     } else {   // no cache set: every expert on the host, nothing fetched
         for (int j = 0; j < k; ++j) {
             hit[j] = 0;
@@ -336,6 +381,8 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
     }
     int nfill = 0;
     for (int j = 0; j < k; ++j) nfill += fill[j] >= 0;
+    if (covered && rt->cache->policy != MOE_POLICY_STATIC)
+        for (int j = 0; j < k; ++j) rt->stats.fills_skipped += !hit[j] && fill[j] < 0;
 
     int nmiss = 0, nhit = 0;
     const void *mslab[MOE_MAX_TOPK];
@@ -371,10 +418,13 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
     }
 
     // Step 2(b): misses on the host thread pool, written where the reduce reads them.
+    // x and y cross through ordinary cached host memory: the coherent buffers the GPU
+    // shares are not what the dot products should re-read for every weight row.
     if (nmiss) {
-        float *yh = rt->h_y + (size_t)layer * d;
         const double t2 = now_ms();
-        rt->pool->expert_ffn(rt->h_x, mslab, mw, nmiss, d, D.f, yh);
+        std::memcpy(rt->x_local.data(), rt->h_x, sizeof(float) * d);
+        rt->pool->expert_ffn(rt->x_local.data(), mslab, mw, nmiss, d, D.f, rt->y_local.data());
+        std::memcpy(rt->h_y + (size_t)layer * d, rt->y_local.data(), sizeof(float) * d);
         rt->stats.host_ffn_ms += now_ms() - t2;
     }
     MOE_HIP(moe::launch_ffn_reduce(p, nmiss ? rt->h_y_dev + (size_t)layer * d : nullptr, out_dev, sc));
@@ -388,6 +438,17 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
         MOE_HIP(hipMemcpyAsync(rt->d_slotmap + (size_t)layer * n, row, sizeof(int32_t) * n, hipMemcpyHostToDevice, sw));
         MOE_HIP(hipEventRecord(rt->ev_fill[layer], sw));
         rt->fill_pending[layer] = 1;
+        if (rt->fill_limit > 0) {
+            hipEvent_t fe = nullptr;
+            if (!rt->fill_spare.empty()) {
+                fe = rt->fill_spare.back();
+                rt->fill_spare.pop_back();
+            } else {
+                MOE_HIP(hipEventCreateWithFlags(&fe, hipEventDisableTiming));
+            }
+            MOE_HIP(hipEventRecord(fe, sw));
+            rt->inflight.emplace_back(fe, nfill);
+        }
     }
 
     rt->stats.layer_calls += 1;
@@ -430,6 +491,14 @@ int moe_runtime_device_slotmap(moe_runtime *rt, int layer, int32_t *slotmap_out)
     if (rt->fill_pending[layer]) MOE_HIP(hipEventSynchronize(rt->ev_fill[layer]));
     MOE_HIP(hipMemcpy(slotmap_out, rt->d_slotmap + (size_t)layer * rt->desc.n, sizeof(int32_t) * rt->desc.n,
                       hipMemcpyDeviceToHost));
+    return MOE_OK;
+}
+
+int moe_runtime_set_fill_limit(moe_runtime *rt, int max_slabs_in_flight)
+{
+    MOE_REQUIRE(rt, "moe_runtime_set_fill_limit: null handle");
+    MOE_REQUIRE(max_slabs_in_flight >= 0, "moe_runtime_set_fill_limit: %d < 0", max_slabs_in_flight);
+    rt->fill_limit = max_slabs_in_flight;
     return MOE_OK;
 }
 

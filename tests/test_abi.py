@@ -155,6 +155,24 @@ def test_library_policies_vs_oracle(policy, n, k, ways):
         c.reset()
 
 
+@pytest.mark.parametrize("policy", ["lru", "fifo"])
+def test_library_masked_insertion_vs_oracle(policy):
+    """Bounded post-fetch: misses that may not be inserted (random masks) give the same
+    slots, hits, fills and evictions as the oracle's masked access."""
+    rng = random.Random(sum(map(ord, policy)))
+    n, k, ways, L = 8, 2, 4, 2
+    c = moe.Cache(L, n, ways, k, policy=policy)
+    ref = olru.LRUCache(L, ways, policy=policy)
+    for t in range(500):
+        for layer in range(L):
+            sel = rng.sample(range(n), k)
+            ins = [rng.random() < 0.4 for _ in sel]
+            slots, hits = c.lookup(layer, sel)
+            fill, ev = c.update_masked(layer, sel, ins)
+            assert (list(slots), list(hits), list(fill), list(ev)) == ref.access(layer, sel, ins)
+            assert list(c.slotmap(layer)) == ref.slotmap(layer, n)
+
+
 def test_static_policy_validation():
     with pytest.raises(moe.MoeError):
         moe.Cache(1, 8, 2, 2, policy="static", static_content=[[1, 1]])      # duplicate

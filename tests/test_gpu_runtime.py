@@ -184,3 +184,43 @@ def test_runtime_mixtral_static_policy():
     worst = _check_trace(world, idx, w, hit, out, 6, {0}, lambda t, l: True)
     assert world.rt.stats()["fills"] == 0
     say("  worst max|err|/RMS", worst)
+
+
+@pytest.mark.parametrize("name,L,T,limit", [("tiny", 1, 64, 1), ("tiny", 3, 24, 2), ("mixtral", 2, 8, 1)])
+def test_runtime_bounded_postfetch(name, L, T, limit):
+    """Bounded post-fetch (at most `limit` slabs in flight): a miss beyond the budget runs
+    on the host and is not inserted. Which misses were inserted depends on copy timing,
+    so it is read back from the cache table after every layer call; replaying the GPU's
+    sets with those insertions through the oracle's masked LRU must reproduce every hit,
+    slot and the device mirror bit for bit, and the outputs stay within tolerance."""
+    oracle.set_threads(min(16, os.cpu_count() or 1))
+    say("runtime bounded post-fetch", name, L, T, limit)
+    world = World(name, L=L, T=T, threads=8)
+    world.rt.set_fill_limit(limit)
+    import torch
+    ref = olru.LRUCache(world.L, world.ways)
+    sc = world.streams
+    worst = 0.0
+    skipped = 0
+    for t in range(T):
+        for l in range(world.L):
+            idx, w, hit = world.rt.layer_forward(l, world.xd[t, l], world.out[t, l], sc)
+            after = world.cache.slotmap(l)
+            inserted = [bool(after[e] >= 0) for e in idx]          # hits stay, inserted misses appear
+            slots, hits, fills, ev = ref.access(l, list(idx), inserted)
+            assert list(hit) == hits, (t, l)
+            assert list(after) == ref.slotmap(l, world.n), (t, l)
+            skipped += sum(1 for h, i in zip(hits, inserted) if not h and not i)
+            if name == "tiny" or t % 3 == 0:
+                torch.cuda.synchronize()
+                oidx, ow = router_parity(idx, w, world.X[l, t], world.wr[l], world.k)
+                o = world.oracle_out(l, t, oidx)
+                worst = max(worst, assert_close(world.out[t, l].cpu().numpy(), o, f"t={t} layer={l}"))
+    torch.cuda.synchronize()
+    world.rt.sync()
+    for l in range(world.L):
+        assert list(world.rt.device_slotmap(l)) == ref.slotmap(l, world.n)
+    st = world.rt.stats()
+    assert st["fills_skipped"] == skipped
+    assert st["fills"] + st["fills_skipped"] == st["expert_misses"]
+    say("  worst max|err|/RMS", worst, "fills", st["fills"], "skipped", skipped)

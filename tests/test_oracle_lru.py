@@ -218,3 +218,34 @@ def test_static_set_never_changes():
         assert s.expert == content
     with pytest.raises(ValueError):
         lru.StaticSet(2, [1, 1])
+
+
+# ---- bounded post-fetch: misses that are not inserted -------------------------------
+
+@pytest.mark.parametrize("k,ways", [(1, 2), (2, 2), (2, 3)])
+def test_masked_insertion_vs_definitional(k, ways):
+    """A miss whose post-fetch is not issued is not inserted. Against the content
+    definition (top-M keys among the old content and the inserted misses) on every
+    length-5 sequence over 4 experts, with random insertion masks."""
+    subs = _subsets(4, k)
+    rng = random.Random(11 * k + ways)
+    for seq in itertools.product(subs, repeat=5):
+        seq = [rng.sample(s_, len(s_)) for s_ in seq]
+        masks = [[rng.random() < 0.5 for _ in s_] for s_ in seq]
+        s = lru.LRUSet(ways)
+        hits = [s.access(sel, ins)[1] for sel, ins in zip(seq, masks)]
+        assert hits == lru.definitional_hits_masked(seq, masks, ways)
+
+
+def test_masked_insertion_extremes():
+    rng = random.Random(5)
+    seq = [rng.sample(range(8), 2) for _ in range(200)]
+    a, b = lru.LRUSet(4), lru.LRUSet(4)
+    for sel in seq:                                   # all allowed == plain LRU
+        assert a.access(sel, [True, True]) == b.access(sel)
+    c = lru.LRUSet(4)
+    c.access([1, 2])
+    for sel in seq:                                   # nothing allowed: content frozen
+        _, hits, fills, ev = c.access(sel, [False, False])
+        assert hits == [e in (1, 2) for e in sel] and fills == [-1, -1] and ev == [-1, -1]
+        assert c.content() == {1, 2}
