@@ -277,6 +277,70 @@ def pcie_study(args, torch, moe, synth, wl):
     return res
 
 
+def small_batch_study(args, torch, moe, synth, wl):
+    """Multi-token decode with every expert resident (T = 1..64 tokens per step): the
+    grouped-GEMM path (prefill kernels at small T) against T single-token passes of the
+    GEMV hit path, per MoE layer. Not in the paper; it locates the GEMV -> GEMM
+    crossover between the decode and prefill kernels."""
+    import numpy as np
+    d, f, n, k = wl.d, wl.f, wl.n, wl.k
+    L = 4                                   # distinct layers so weights are not reused from cache
+    stride = moe.slab_bytes(d, f)
+    pool = torch.empty(L * n * stride, dtype=torch.uint8, device="cuda")
+    for l in range(L):
+        for e in range(n):
+            t = pool[(l * n + e) * stride:(l * n + e) * stride + 3 * d * f * 2].view(torch.bfloat16)
+            synth.expert_slab_torch(synth.seed_for(args.seed, wl.name, "expert", l, e), d, f, wl.w_std, out=t)
+    wr = torch.stack([synth.router_weights_torch(synth.seed_for(args.seed, wl.name, "router", l), n, d)
+                      for l in range(L)]).contiguous()
+    Tmax = 64
+    X = torch.from_numpy(synth.iid_states(synth.seed_for(args.seed, wl.name, "prompt"), Tmax, d)).cuda()
+    out = torch.empty((Tmax, d), device="cuda")
+    ws = torch.empty(moe.prefill_workspace_bytes(d, f, n, k, Tmax), dtype=torch.uint8, device="cuda")
+    # single-token GEMV path over resident experts: slot s of layer l holds expert s
+    fws = torch.empty(moe.ffn_workspace_bytes(k, d, f), dtype=torch.uint8, device="cuda")
+    idx = torch.empty((Tmax, k), dtype=torch.int32, device="cuda")
+    wts = torch.empty((Tmax, k), dtype=torch.float32, device="cuda")
+    y = torch.empty(d, device="cuda")
+
+    def time_it(fn, reps=5):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    rows = []
+    for T in (1, 2, 4, 8, 16, 32, 64):
+        def grouped():
+            for l in range(L):
+                moe.prefill_forward(X[:T], wr[l], pool[l * n * stride:(l + 1) * n * stride], d, f, n, k, out[:T], ws)
+
+        def gemv():
+            for l in range(L):
+                moe.router_topk(X[:T], wr[l], k, idx_out=idx[:T], w_out=wts[:T])
+                for t in range(T):
+                    moe.expert_ffn_hits(X[t], pool[l * n * stride:(l + 1) * n * stride], n, idx[t], wts[t], d, f, y,
+                                        fws)
+        g_us = time_it(grouped) / L
+        v_us = time_it(gemv, reps=2 if T >= 16 else 5) / L
+        touched = int(np.unique(idx[:T].cpu().numpy()).size)
+        rows.append({"T": T, "grouped_us_per_layer": round(g_us, 1), "gemv_us_per_layer": round(v_us, 1),
+                     "experts_touched": touched,
+                     "grouped_weight_GBs": round(touched * 3 * d * f * 2 / (g_us * 1e-6) / 1e9, 1)})
+        log(json.dumps(rows[-1]))
+    return {
+        "metric": "multi-token decode, all experts resident: us per MoE layer, grouped GEMM vs per-token GEMV",
+        "value": None, "unit": "us per layer", "n_gpus": 1, "higher_is_better": False, "data": "synthetic",
+        "config": {"workload": wl.desc, "layers_timed": L, "tokens": "i.i.d. N(0,1)"},
+        "rows": rows,
+    }
+
+
 def measured_traffic(args):
     """HBM bytes per k_gate_up launch from the committed PMC record, if it was taken on
     the current kernel source and the same workload arguments; else None."""
@@ -379,6 +443,8 @@ def main():
     ap.add_argument("--hit-study", action="store_true",
                     help="only replay router selections through LRU/FIFO/static caches of several sizes")
     ap.add_argument("--pcie", action="store_true", help="only measure host-to-device expert copies")
+    ap.add_argument("--small-batch", action="store_true",
+                    help="only time multi-token decode (T = 1..64) with every expert resident")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB 5 times (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -404,6 +470,9 @@ def main():
         print(json.dumps({"copy_calibration_bytes_read": nbytes, "copy_calibration_bytes_written": nbytes}))
         return
     wl = synth.WORKLOADS[args.workload]
+    if args.small_batch:
+        print(json.dumps(small_batch_study(args, torch, moe, synth, wl)), flush=True)
+        return
     if args.pcie:
         print(json.dumps(pcie_study(args, torch, moe, synth, wl)), flush=True)
         return
