@@ -36,6 +36,7 @@ constexpr int kThreads = 256;
 constexpr int kBK = 64;         // K per stage
 constexpr int kLdsStride = kBK + 8;   // bf16 per LDS row (16-byte pad against bank conflicts)
 constexpr int kXcds = 8;
+constexpr int kSpreadTokens = 64;   // below this many (token, expert) pairs per expert, spread items over XCDs
 constexpr int kMaxDownSplits = 4;
 
 __device__ __forceinline__ uint16_t f2bf(float f)
@@ -125,7 +126,8 @@ struct GemmArgs {
     int mtiles;               // M tiles per expert (upper bound)
     int ntiles;               // N tiles per matrix
     int ksplit;               // K splits
-    int per_xcd;              // work items per XCD
+    int per_xcd;              // work items per XCD (expert-per-XCD layout)
+    int spread;               // 1: item b is simply the b-th (expert, m, n, k) item
     uint16_t *h;              // gate/up output, bf16 [P][f]
     float *yp;                // down output, fp32 [ksplit][P][d]
 };
@@ -164,11 +166,16 @@ __global__ __launch_bounds__(kGThreads) void k_moe_gemm(GemmArgs g)
 {
     __shared__ uint16_t lds_a[2][kTileM * kLdsStride];
 
-    const int xcd = blockIdx.x % kXcds;
-    int q = blockIdx.x / kXcds;
-    if (q >= g.per_xcd) return;
     const int per_expert = g.mtiles * g.ntiles * g.ksplit;
-    const int e = xcd + kXcds * (q / per_expert);
+    int q, e;
+    if (g.spread) {   // few tokens per expert: an expert's items go round all XCDs
+        q = blockIdx.x;
+        e = q / per_expert;
+    } else {          // an expert's items stay on XCD e mod 8, sharing its token rows in L2
+        q = blockIdx.x / kXcds;
+        if (q >= g.per_xcd) return;
+        e = blockIdx.x % kXcds + kXcds * (q / per_expert);
+    }
     if (e >= g.n) return;
     q %= per_expert;
     const int ks = q % g.ksplit;
@@ -396,13 +403,19 @@ hipError_t launch_prefill(const PrefillPlan &P, const float *X, float *OUT, int3
     g.h = ws.h;
     g.yp = ws.yp;
     const int groups = (P.n + kXcds - 1) / kXcds;
+    // With few tokens per expert most experts are idle or nearly so, and keeping an
+    // expert on one XCD would leave the others without work; spread its tiles instead.
+    g.spread = (int64_t)P.T * P.k < (int64_t)kSpreadTokens * P.n;
+    auto grid_of = [&](const GemmArgs &a) {
+        return g.spread ? P.n * a.mtiles * a.ntiles * a.ksplit : kXcds * a.per_xcd;
+    };
 
     // gate/up: each work group covers 128 columns of H (128 W1 rows + the same 128 W3 rows), K = d
     g.a = ws.xb;
     g.ntiles = P.f / 128;
     g.ksplit = 1;
     g.per_xcd = groups * g.mtiles * g.ntiles * g.ksplit;
-    hipLaunchKernelGGL((k_moe_gemm<true, 2, 2>), dim3(kXcds * g.per_xcd), dim3(kGThreads), 0, s, g);
+    hipLaunchKernelGGL((k_moe_gemm<true, 2, 2>), dim3(grid_of(g)), dim3(kGThreads), 0, s, g);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     // down: 256 (or 128) output rows per work group, K = f split in 4 (or 2) parts
@@ -411,8 +424,8 @@ hipError_t launch_prefill(const PrefillPlan &P, const float *X, float *OUT, int3
     const bool wide = P.d % 256 == 0;
     g.ntiles = P.d / (wide ? 256 : 128);
     g.per_xcd = groups * g.mtiles * g.ntiles * g.ksplit;
-    if (wide) hipLaunchKernelGGL((k_moe_gemm<false, 4, 2>), dim3(kXcds * g.per_xcd), dim3(kGThreads), 0, s, g);
-    else hipLaunchKernelGGL((k_moe_gemm<false, 4, 1>), dim3(kXcds * g.per_xcd), dim3(kGThreads), 0, s, g);
+    if (wide) hipLaunchKernelGGL((k_moe_gemm<false, 4, 2>), dim3(grid_of(g)), dim3(kGThreads), 0, s, g);
+    else hipLaunchKernelGGL((k_moe_gemm<false, 4, 1>), dim3(grid_of(g)), dim3(kGThreads), 0, s, g);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     const int nparts = (P.d + 4 * kThreads - 1) / (4 * kThreads);
