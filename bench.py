@@ -32,7 +32,8 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def build_world(torch, moe, synth, wl, steps_total, seed, threads, pinned_gb, policy="lru", budget_gb=None):
+def build_world(torch, moe, synth, wl, steps_total, seed, threads, pinned_gb, policy="lru", budget_gb=None,
+                ways=None):
     """Device cache, pinned host experts, router weights and hidden states.
 
     Page-locked host memory is capped per process on the GPU hosts (64 GiB), below
@@ -41,7 +42,7 @@ def build_world(torch, moe, synth, wl, steps_total, seed, threads, pinned_gb, po
     and layer l uses host layer l mod H (its router and its cache slots stay its own).
     """
     import numpy as np
-    d, f, n, k, L, M = wl.d, wl.f, wl.n, wl.k, wl.L, wl.ways
+    d, f, n, k, L, M = wl.d, wl.f, wl.n, wl.k, wl.L, (ways or wl.ways)
     stride = moe.slab_bytes(d, f)
     per_layer = n * stride
     H = max(1, min(L, int(pinned_gb * 2**30) // per_layer))
@@ -436,6 +437,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--policy", default="lru", choices=["lru", "fifo", "static"],
                     help="cache replacement policy (Section IV-D; the paper's is LRU)")
+    ap.add_argument("--ways", type=int, default=0,
+                    help="cache slots per layer (default: the workload's; = experts for an all-resident cache)")
     ap.add_argument("--budget-gb", type=float, default=None,
                     help="GPU memory for the expert cache (GB); layers past the covered ones run on the host")
     ap.add_argument("--fill-limit", type=int, default=0,
@@ -485,7 +488,7 @@ def main():
     steps_total = args.warmup + args.steps
     assert steps_total <= wl.T, f"at most {wl.T} decode steps in this workload"
     world = build_world(torch, moe, synth, wl, steps_total, args.seed, args.threads, args.pinned_gb,
-                        policy=args.policy, budget_gb=args.budget_gb)
+                        policy=args.policy, budget_gb=args.budget_gb, ways=args.ways or None)
     rt, xd = world["rt"], world["xd"]
     rt.set_fill_limit(args.fill_limit)
     L, k, d = wl.L, wl.k, wl.d
@@ -536,7 +539,7 @@ def main():
         "config": {
             "workload": wl.desc,
             "d_model": wl.d, "d_ffn": wl.f, "experts": wl.n, "top_k": wl.k, "layers": wl.L,
-            "cache_ways": wl.ways, "shared_d_ffn": wl.f_shared, "batch": 1,
+            "cache_ways": args.ways or wl.ways, "shared_d_ffn": wl.f_shared, "batch": 1,
             "weights": "bf16, fp32 accumulate", "cache_start": f"cold, {args.warmup} warmup tokens",
             "host_threads": world["hp"].threads, "parallelism": "single GPU",
             "host_expert_layers_distinct": world["H"],

@@ -40,6 +40,7 @@ def _ffn(torch, x, pool, n_slots, slots, w, d, f, k_ws=None):
     (1024, 4104, 2, [1, 0]),          # several down segments with a ragged tail
     (512, 1024, 8, [7, 0, 3, 5, 1, 2, 6, 4]),   # eight jobs
     (4096, 256, 2, [0, 1]),           # short reduction, wide rows
+    (8192, 1032, 16, list(range(15, -1, -1))),   # the ABI maxima: d = MOE_MAX_D, 16 jobs
 ])
 def test_hits_parity(d, f, nslots, slots):
     torch = torch_cuda()
