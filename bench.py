@@ -443,6 +443,8 @@ def main():
                     help="GPU memory for the expert cache (GB); layers past the covered ones run on the host")
     ap.add_argument("--fill-limit", type=int, default=0,
                     help="bounded post-fetch: at most this many expert slabs in flight (0: every miss fetched)")
+    ap.add_argument("--nonblocking", action="store_true",
+                    help="never wait for a post-fetch: experts whose copy has not landed run on the host")
     ap.add_argument("--hit-study", action="store_true",
                     help="only replay router selections through LRU/FIFO/static caches of several sizes")
     ap.add_argument("--pcie", action="store_true", help="only measure host-to-device expert copies")
@@ -491,6 +493,7 @@ def main():
                         policy=args.policy, budget_gb=args.budget_gb, ways=args.ways or None)
     rt, xd = world["rt"], world["xd"]
     rt.set_fill_limit(args.fill_limit)
+    rt.set_nonblocking(args.nonblocking)
     L, k, d = wl.L, wl.k, wl.d
     out = torch.empty((2, L, d), dtype=torch.float32, device="cuda")
     streams = (torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream())
@@ -545,7 +548,8 @@ def main():
             "host_expert_layers_distinct": world["H"],
             "cache_policy": world["policy"], "covered_layers": world["covered"],
             "post_fetch": (f"at most {args.fill_limit} slabs in flight" if args.fill_limit
-                           else "every miss (Section III-A step 3)"),
+                           else "every miss (Section III-A step 3)")
+                          + ("; non-blocking (in flight => host)" if args.nonblocking else "; parity (waits)"),
         },
         "roofline": {
             "kernel": "k_gate_up (W1/W3 rows + SiLU*mul)",
@@ -574,6 +578,7 @@ def main():
             "route_wait_ms_per_token": round(st["route_wait_ms"] / K, 3),
             "fills_per_token": round(st["fills"] / K, 3),
             "fills_skipped_per_token": round(st["fills_skipped"] / K, 3),
+            "inflight_misses_per_token": round(st["inflight_misses"] / K, 3),
         },
     }
     log(json.dumps(result["trace"]), json.dumps(result["hit_ffn"]))
@@ -581,7 +586,7 @@ def main():
         "what": f"host FFN of one layer's {k} experts (all missed), alone, by thread count",
         "by_threads": host_sweep(moe, wl, world)}
     log(json.dumps(result["host_expert_layer"]))
-    if args.fill_limit == 0 and world["policy"] != "static" and world["covered"] > 0:
+    if args.fill_limit == 0 and not args.nonblocking and world["policy"] != "static" and world["covered"] > 0:
         # The same tokens once more, cold cache, with bounded post-fetch (at most two
         # slabs in flight): misses beyond that run on the host without being fetched.
         rt.close()

@@ -241,7 +241,8 @@ void moe_runtime_destroy(moe_runtime *rt);
  * x_dev    device fp32 [d] hidden state; out_dev device fp32 [d] routed-expert output
  *          (+ shared expert).
  * idx_host host int32 [k], w_host host fp32 [k]: routing in rank order (nullable).
- * hit_host host uint8 [k]: 1 if the expert was a cache hit (nullable).
+ * hit_host host uint8 [k]: 1 if the expert ran on the GPU as a cache hit (nullable); in
+ *          parity mode exactly the cache hits.
  * compute_stream runs the router, hit FFN and combine; copy_stream the post-fetch of
  * missed experts. act_stream is accepted for ABI stability and may be NULL: the
  * router kernel itself writes the routing and the hidden state into coherent pinned
@@ -274,7 +275,21 @@ int moe_decode_step(moe_runtime *rt, const float *x_dev, float *out_dev, int32_t
  */
 int moe_runtime_set_fill_limit(moe_runtime *rt, int max_slabs_in_flight);
 
-/* Blocks until every copy the runtime enqueued has finished. */
+/*
+ * Non-blocking post-fetch (enable != 0). By default (parity mode) a layer call whose set
+ * still has a post-fetch in flight makes the compute stream wait for it, so a fetched
+ * expert is used from the next token on and the hit/miss sequence does not depend on
+ * timing. In non-blocking mode the call does not wait: experts whose copy has not
+ * landed are run on the host for that call ("in flight => miss"); the cache table
+ * (moe_cache_*) evolves exactly as in parity mode, only where experts run differs.
+ * hit_host reports where each expert ran (1 = GPU).
+ */
+int moe_runtime_set_nonblocking(moe_runtime *rt, int enable);
+
+/*
+ * Blocks until every copy the runtime enqueued has finished and the device mirror holds
+ * every landed post-fetch (synchronises the device).
+ */
 int moe_runtime_sync(moe_runtime *rt);
 
 /* Device expert->slot mirror of one layer copied to host [n] (synchronous). */
@@ -296,6 +311,8 @@ typedef struct moe_runtime_stats {
     double down_ms;
     double down_bytes;
     int64_t fills_skipped;    /* misses not post-fetched because of the fill limit */
+    int64_t inflight_misses;  /* cache hits run on the host because their post-fetch had
+                                 not landed (non-blocking mode) */
 } moe_runtime_stats;
 
 /*

@@ -290,6 +290,9 @@ class Runtime:
     def set_timing(self, on: bool):
         _check("moe_runtime_set_timing", _lib.moe_runtime_set_timing(self.handle, 1 if on else 0))
 
+    def set_nonblocking(self, enable=True):
+        _check("moe_runtime_set_nonblocking", _lib.moe_runtime_set_nonblocking(self.handle, int(bool(enable))))
+
     def set_fill_limit(self, max_slabs_in_flight):
         _check("moe_runtime_set_fill_limit", _lib.moe_runtime_set_fill_limit(self.handle, int(max_slabs_in_flight)))
 

@@ -35,7 +35,7 @@ class RuntimeStats(ctypes.Structure):
         ("host_ffn_ms", c_double), ("route_wait_ms", c_double),
         ("gate_up_launches", ctypes.c_int64), ("gate_up_ms", c_double), ("gate_up_bytes", c_double),
         ("down_launches", ctypes.c_int64), ("down_ms", c_double), ("down_bytes", c_double),
-        ("fills_skipped", ctypes.c_int64),
+        ("fills_skipped", ctypes.c_int64), ("inflight_misses", ctypes.c_int64),
     ]
 
 
@@ -79,6 +79,7 @@ SIGNATURES = [
     ("moe_runtime_sync", c_int, [c_void_p]),
     ("moe_runtime_device_slotmap", c_int, [c_void_p, c_int, c_i32p]),
     ("moe_runtime_set_fill_limit", c_int, [c_void_p, c_int]),
+    ("moe_runtime_set_nonblocking", c_int, [c_void_p, c_int]),
     ("moe_runtime_set_timing", c_int, [c_void_p, c_int]),
     ("moe_runtime_get_stats", c_int, [c_void_p, ctypes.POINTER(RuntimeStats)]),
     ("moe_runtime_reset_stats", c_int, [c_void_p]),

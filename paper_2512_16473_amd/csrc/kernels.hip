@@ -341,8 +341,13 @@ __global__ __launch_bounds__(kBlock) void k_combine(const float *a, const float 
 template <int CPR>
 __global__ __launch_bounds__(kRouterBlock) void k_router(const float *X, const float *Wr, int d, int n, int k,
                                                          int32_t *idx, float *wout, RouteMailbox *mbox,
-                                                         float *x_host, int32_t seq)
+                                                         float *x_host, int32_t seq, const int32_t *row_src,
+                                                         int32_t *row_dst)
 {
+    // Decode only: install the layer's expert->slot mirror row that the hit kernels after
+    // this one read (the host's view of which slots hold landed experts).
+    if (row_src)
+        for (int i = threadIdx.x; i < n; i += kRouterBlock) row_dst[i] = row_src[i];
     constexpr int kWaves = kRouterBlock / kWave;
     __shared__ double logit[MOE_MAX_EXPERTS];
     __shared__ float4 xs[CPR * kWave];
@@ -507,10 +512,12 @@ hipError_t launch_gate_up(const FfnParams &p, int items, hipStream_t s, hipEvent
 
 template <int CPR>
 hipError_t launch_router_cpr(const float *x, const float *wr, int T, int d, int n, int k, int32_t *idx, float *w,
-                             hipStream_t s, RouteMailbox *mbox, float *x_host, int32_t seq)
+                             hipStream_t s, RouteMailbox *mbox, float *x_host, int32_t seq, const int32_t *row_src,
+                             int32_t *row_dst)
 {
     clear_launch_error();
-    hipLaunchKernelGGL(k_router<CPR>, dim3(T), dim3(kRouterBlock), 0, s, x, wr, d, n, k, idx, w, mbox, x_host, seq);
+    hipLaunchKernelGGL(k_router<CPR>, dim3(T), dim3(kRouterBlock), 0, s, x, wr, d, n, k, idx, w, mbox, x_host, seq,
+                       row_src, row_dst);
     return hipGetLastError();
 }
 
@@ -555,13 +562,15 @@ void ffn_bind_workspace(FfnParams &p, void *ws, int max_jobs, int d, int f_max)
 }
 
 hipError_t launch_router(const float *x, const float *wr, int T, int d, int n, int k, int32_t *idx,
-                         float *w, hipStream_t s, RouteMailbox *mbox, float *x_host, int32_t seq)
+                         float *w, hipStream_t s, RouteMailbox *mbox, float *x_host, int32_t seq,
+                         const int32_t *row_src, int32_t *row_dst)
 {
     if (T <= 0) return hipSuccess;
-    if (T != 1) mbox = nullptr, x_host = nullptr;
+    if (T != 1) mbox = nullptr, x_host = nullptr, row_src = nullptr;
+    if (!row_dst) row_src = nullptr;
     const int cpr = (d / 4 + kWave - 1) / kWave;
 #define MOE_CPR_CASE(N) \
-    if (cpr <= N) return launch_router_cpr<N>(x, wr, T, d, n, k, idx, w, s, mbox, x_host, seq);
+    if (cpr <= N) return launch_router_cpr<N>(x, wr, T, d, n, k, idx, w, s, mbox, x_host, seq, row_src, row_dst);
     MOE_CPR_CASE(1) MOE_CPR_CASE(2) MOE_CPR_CASE(4) MOE_CPR_CASE(8) MOE_CPR_CASE(16) MOE_CPR_CASE(32)
 #undef MOE_CPR_CASE
     return hipErrorInvalidValue;

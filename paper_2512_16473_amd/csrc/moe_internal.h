@@ -58,9 +58,12 @@ struct RouteMailbox {
 };
 
 // mbox/x_host (device addresses of host memory, nullable) are only used when T == 1.
+// row_src (device address of host memory, nullable; T == 1 only): n int32 copied to
+// row_dst by the kernel before it exits, i.e. before any later kernel on the stream.
 hipError_t launch_router(const float *x, const float *wr, int T, int d, int n, int k,
                          int32_t *idx, float *w, hipStream_t s, RouteMailbox *mbox = nullptr,
-                         float *x_host = nullptr, int32_t seq = 0);
+                         float *x_host = nullptr, int32_t seq = 0, const int32_t *row_src = nullptr,
+                         int32_t *row_dst = nullptr);
 // gate/up/SiLU then down; `after_down` (nullable) is recorded right after the down kernel.
 hipError_t launch_ffn_stream(const FfnParams &p, hipStream_t s, const FfnEvents *ev,
                              hipEvent_t after_down);

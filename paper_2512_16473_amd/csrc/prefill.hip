@@ -153,17 +153,17 @@ struct GemmArgs {
 // rows (kNB = 1 when d is not a multiple of 256); K = f is split in ksplit parts that write
 // separate fp32 partial sums.
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
-constexpr int kGThreads = 512;
-constexpr int kGWaves = kGThreads / 64;
+constexpr int kGWaves = 8;                             // waves per work group of the launches below
 constexpr int kMBlocks = 12;                           // 16-token blocks per tile
 constexpr int kTileM = kMBlocks * 16;                  // 192 tokens
-constexpr int kANum = kTileM * 8 / kGThreads;          // token-tile 16-byte chunks per thread per step
 constexpr int kKBlocks = kBK / 32;                     // MFMA K blocks per step
-static_assert(kTileM * 8 % kGThreads == 0, "token tile must split evenly over the threads");
 
-template <bool kGateUp, int kS, int kNB>
-__global__ __launch_bounds__(kGThreads) void k_moe_gemm(GemmArgs g)
+template <bool kGateUp, int kS, int kNB, int kWaves>
+__global__ __launch_bounds__(kWaves * 64) void k_moe_gemm(GemmArgs g)
 {
+    constexpr int kThr = kWaves * 64;
+    constexpr int kAN = kTileM * 8 / kThr;             // token-tile 16-byte chunks per thread per step
+    static_assert(kTileM * 8 % kThr == 0, "token tile must split evenly over the threads");
     __shared__ uint16_t lds_a[2][kTileM * kLdsStride];
 
     const int per_expert = g.mtiles * g.ntiles * g.ksplit;
@@ -198,28 +198,28 @@ __global__ __launch_bounds__(kGThreads) void k_moe_gemm(GemmArgs g)
     // this lane's weight rows (MFMA column lane mod 16 of each column block) and K offset
     const uint16_t *bsrc[kNB];
     if constexpr (kGateUp) {
-        const size_t wrow = (size_t)nt * 128 + wv * 16 + (lane & 15);
+        const size_t wrow = (size_t)nt * (kWaves * 16) + wv * 16 + (lane & 15);
         bsrc[0] = w + wrow * g.d + k0 + 8 * (lane >> 4);
         bsrc[1] = w + (size_t)g.f * g.d + wrow * g.d + k0 + 8 * (lane >> 4);
     } else {
 #pragma unroll
         for (int nb = 0; nb < kNB; ++nb) {
-            const size_t wrow = (size_t)nt * (kGWaves * 16 * kNB) + wv * 16 * kNB + nb * 16 + (lane & 15);
+            const size_t wrow = (size_t)nt * (kWaves * 16 * kNB) + wv * 16 * kNB + nb * 16 + (lane & 15);
             bsrc[nb] = w + (size_t)2 * g.f * g.d + wrow * g.f + k0 + 8 * (lane >> 4);
         }
     }
     // token-tile chunks staged by this thread: chunk c = tid + 512 i is row c / 8, 16-byte column c % 8
-    const uint16_t *asrc[kANum];
+    const uint16_t *asrc[kAN];
 #pragma unroll
-    for (int i = 0; i < kANum; ++i) {
-        const int c = tid + kGThreads * i;
+    for (int i = 0; i < kAN; ++i) {
+        const int c = tid + kThr * i;
         const int r = c >> 3, col = (c & 7) * 8;
         const int rr = r < rows ? r : 0;
         if (kGateUp) asrc[i] = g.a + (size_t)(g.perm[row0 + rr] / g.k) * g.d + k0 + col;
         else asrc[i] = g.a + (size_t)(row0 + rr) * g.f + k0 + col;
     }
 
-    u32x4_t ra[kS][kANum], rb[kS][kNB * kKBlocks];
+    u32x4_t ra[kS][kAN], rb[kS][kNB * kKBlocks];
     floatx4_t acc[kMBlocks][kNB];
 #pragma unroll
     for (int m = 0; m < kMBlocks; ++m)
@@ -229,7 +229,7 @@ __global__ __launch_bounds__(kGThreads) void k_moe_gemm(GemmArgs g)
 #define MOE_LOAD(set, step)                                                                           \
     do {                                                                                              \
         const int ko_ = min((step), nsteps - 1) * kBK;                                                \
-        _Pragma("unroll") for (int i = 0; i < kANum; ++i) ra[set][i] =                                \
+        _Pragma("unroll") for (int i = 0; i < kAN; ++i) ra[set][i] =                                \
             *reinterpret_cast<const u32x4_t *>(asrc[i] + ko_);                                        \
         _Pragma("unroll") for (int nb = 0; nb < kNB; ++nb)                                            \
         _Pragma("unroll") for (int kb = 0; kb < kKBlocks; ++kb) rb[set][nb * kKBlocks + kb] =         \
@@ -237,8 +237,8 @@ __global__ __launch_bounds__(kGThreads) void k_moe_gemm(GemmArgs g)
     } while (0)
 #define MOE_STASH(set, buf)                                                                           \
     do {                                                                                              \
-        _Pragma("unroll") for (int i = 0; i < kANum; ++i) {                                           \
-            const int c_ = tid + kGThreads * i;                                                       \
+        _Pragma("unroll") for (int i = 0; i < kAN; ++i) {                                           \
+            const int c_ = tid + kThr * i;                                                       \
             *reinterpret_cast<u32x4_t *>(&lds_a[buf][(c_ >> 3) * kLdsStride + (c_ & 7) * 8]) = ra[set][i]; \
         }                                                                                             \
     } while (0)
@@ -286,9 +286,9 @@ __global__ __launch_bounds__(kGThreads) void k_moe_gemm(GemmArgs g)
             if constexpr (kGateUp) {
                 const float gv = acc[m][0][r], uv = acc[m][kNB - 1][r];
                 const float hv = gv / (1.0f + expf(-gv)) * uv;
-                g.h[(size_t)(row0 + tr) * g.f + nt * 128 + wv * 16 + (lane & 15)] = f2bf(hv);
+                g.h[(size_t)(row0 + tr) * g.f + nt * (kWaves * 16) + wv * 16 + (lane & 15)] = f2bf(hv);
             } else {
-                float *dst = g.yp + ((size_t)ks * P + row0 + tr) * g.d + nt * (kGWaves * 16 * kNB) + wv * 16 * kNB +
+                float *dst = g.yp + ((size_t)ks * P + row0 + tr) * g.d + nt * (kWaves * 16 * kNB) + wv * 16 * kNB +
                              (lane & 15);
 #pragma unroll
                 for (int nb = 0; nb < kNB; ++nb) dst[16 * nb] = acc[m][nb][r];
@@ -412,20 +412,20 @@ hipError_t launch_prefill(const PrefillPlan &P, const float *X, float *OUT, int3
 
     // gate/up: each work group covers 128 columns of H (128 W1 rows + the same 128 W3 rows), K = d
     g.a = ws.xb;
-    g.ntiles = P.f / 128;
+    g.ntiles = P.f / (kGWaves * 16);
     g.ksplit = 1;
     g.per_xcd = groups * g.mtiles * g.ntiles * g.ksplit;
-    hipLaunchKernelGGL((k_moe_gemm<true, 2, 2>), dim3(grid_of(g)), dim3(kGThreads), 0, s, g);
+    hipLaunchKernelGGL((k_moe_gemm<true, 2, 2, kGWaves>), dim3(grid_of(g)), dim3(kGWaves * 64), 0, s, g);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     // down: 256 (or 128) output rows per work group, K = f split in 4 (or 2) parts
     g.a = ws.h;
     g.ksplit = down_splits(P.f);
-    const bool wide = P.d % 256 == 0;
-    g.ntiles = P.d / (wide ? 256 : 128);
+    const bool wide = P.d % (kGWaves * 32) == 0;
+    g.ntiles = P.d / (kGWaves * 16 * (wide ? 2 : 1));
     g.per_xcd = groups * g.mtiles * g.ntiles * g.ksplit;
-    if (wide) hipLaunchKernelGGL((k_moe_gemm<false, 4, 2>), dim3(grid_of(g)), dim3(kGThreads), 0, s, g);
-    else hipLaunchKernelGGL((k_moe_gemm<false, 4, 1>), dim3(grid_of(g)), dim3(kGThreads), 0, s, g);
+    if (wide) hipLaunchKernelGGL((k_moe_gemm<false, 4, 2, kGWaves>), dim3(grid_of(g)), dim3(kGWaves * 64), 0, s, g);
+    else hipLaunchKernelGGL((k_moe_gemm<false, 4, 1, kGWaves>), dim3(grid_of(g)), dim3(kGWaves * 64), 0, s, g);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     const int nparts = (P.d + 4 * kThreads - 1) / (4 * kThreads);

@@ -68,11 +68,17 @@ struct moe_runtime {
     float *h_y = nullptr, *h_y_dev = nullptr;   // [L][d] host-path output per layer
     std::vector<float> x_local, y_local;        // [d] cached host copies for the host FFN
     int32_t seq = 0;
-    // pinned staging of the mirror rows for the copy stream
-    int32_t *h_slotmap = nullptr;   // [L][n]
+    // Device mirror of the slot table. Its rows are installed by the layer's router
+    // kernel from coherent host memory (h_rows), so the hit kernels of a layer call see
+    // exactly the row the host decided on for that call. dev_row is the host's copy of
+    // what the device holds: a slot appears there only once its post-fetch has landed.
+    int32_t *h_rows = nullptr, *h_rows_dev = nullptr;   // [L][n]
+    std::vector<int32_t> dev_row;                        // [L][n]
+    std::vector<std::vector<std::pair<int32_t, int32_t>>> pend_fill;   // [L] (expert, slot) in flight
+    std::vector<std::vector<int32_t>> pend_inval;       // [L] evicted experts to drop at the next call
+    bool nonblocking = false;
 
-    hipEvent_t ev_hits = nullptr;
-    std::vector<hipEvent_t> ev_fill;   // [L]
+    std::vector<hipEvent_t> ev_fill;   // [L] after the layer's latest slab copies
     std::vector<char> fill_pending;    // [L]
 
     // Bounded post-fetch: at most fill_limit slabs queued on the copy stream (0: no
@@ -101,7 +107,7 @@ void release(moe_runtime *rt)
     for (auto e : rt->fill_spare) (void)hipEventDestroy(e);
     for (auto e : rt->ev_fill)
         if (e) (void)hipEventDestroy(e);
-    if (rt->ev_hits) (void)hipEventDestroy(rt->ev_hits);
+
     if (rt->d_slotmap) (void)hipFree(rt->d_slotmap);
     if (rt->d_idx) (void)hipFree(rt->d_idx);
     if (rt->d_w) (void)hipFree(rt->d_w);
@@ -109,7 +115,7 @@ void release(moe_runtime *rt)
     if (rt->mbox) (void)hipHostFree(rt->mbox);
     if (rt->h_x) (void)hipHostFree(rt->h_x);
     if (rt->h_y) (void)hipHostFree(rt->h_y);
-    if (rt->h_slotmap) (void)hipHostFree(rt->h_slotmap);
+    if (rt->h_rows) (void)hipHostFree(rt->h_rows);
     delete rt;
 }
 
@@ -233,8 +239,10 @@ int moe_runtime_create(const moe_layer_desc *desc, moe_runtime **out)
         return fail(e, "hipHostGetDevicePointer");
     if ((e = hipHostGetDevicePointer((void **)&rt->h_y_dev, rt->h_y, 0)) != hipSuccess)
         return fail(e, "hipHostGetDevicePointer");
-    if ((e = hipHostMalloc((void **)&rt->h_slotmap, sizeof(int32_t) * nh, 0)) != hipSuccess)
-        return fail(e, "hipHostMalloc");
+    if ((e = hipHostMalloc((void **)&rt->h_rows, sizeof(int32_t) * nh, coherent)) != hipSuccess)
+        return fail(e, "hipHostMalloc(rows)");
+    if ((e = hipHostGetDevicePointer((void **)&rt->h_rows_dev, rt->h_rows, 0)) != hipSuccess)
+        return fail(e, "hipHostGetDevicePointer");
     // Slots the cache holds already (static content, warm cache) get their slabs now.
     for (int l = 0; l < c->layers; ++l)
         for (int sl = 0; sl < D.ways; ++sl) {
@@ -246,14 +254,14 @@ int moe_runtime_create(const moe_layer_desc *desc, moe_runtime **out)
                 return fail(e, "hipMemcpy(initial slot)");
         }
     // Mirror of the host table as it stands now; uncovered layers map nothing.
-    for (int l = 0; l < D.n_layers; ++l) {
-        int32_t *row = rt->h_slotmap + (size_t)l * D.n;
-        if (l < c->layers) std::memcpy(row, &c->where[(size_t)l * D.n], sizeof(int32_t) * D.n);
-        else std::fill(row, row + D.n, -1);
-    }
-    if ((e = hipMemcpy(rt->d_slotmap, rt->h_slotmap, sizeof(int32_t) * nh, hipMemcpyHostToDevice)) != hipSuccess)
+    rt->dev_row.assign(nh, -1);
+    for (int l = 0; l < c->layers; ++l)
+        std::memcpy(&rt->dev_row[(size_t)l * D.n], &c->where[(size_t)l * D.n], sizeof(int32_t) * D.n);
+    std::memcpy(rt->h_rows, rt->dev_row.data(), sizeof(int32_t) * nh);
+    if ((e = hipMemcpy(rt->d_slotmap, rt->h_rows, sizeof(int32_t) * nh, hipMemcpyHostToDevice)) != hipSuccess)
         return fail(e, "hipMemcpy(slotmap)");
-    if ((e = hipEventCreateWithFlags(&rt->ev_hits, hipEventDisableTiming)) != hipSuccess) return fail(e, "event");
+    rt->pend_fill.assign(D.n_layers, {});
+    rt->pend_inval.assign(D.n_layers, {});
     rt->ev_fill.assign(D.n_layers, nullptr);
     rt->fill_pending.assign(D.n_layers, 0);
     for (int l = 0; l < D.n_layers; ++l)
@@ -283,23 +291,40 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
     hipStream_t sc = (hipStream_t)compute_stream, sw = (hipStream_t)copy_stream;
     const int d = D.d, n = D.n, k = D.k;
 
-    // The previous post-fetch into this set (slabs and mirror row) must be complete
-    // before this token routes through the layer; skip the wait once it is.
+    // This call's mirror row: experts evicted at the previous call leave it; post-fetches
+    // into this set join it once they have landed. In parity mode an unfinished
+    // post-fetch is waited for (the compute stream waits on its event); in non-blocking
+    // mode its experts stay out of the row and run on the host this time.
+    int32_t *row = &rt->dev_row[(size_t)layer * n];
+    bool install = !rt->pend_inval[layer].empty();
+    for (const int32_t v : rt->pend_inval[layer]) row[v] = -1;
+    rt->pend_inval[layer].clear();
     if (rt->fill_pending[layer]) {
         const hipError_t q = hipEventQuery(rt->ev_fill[layer]);
-        if (q == hipSuccess) {
-            rt->fill_pending[layer] = 0;
-        } else {
-            if (q != hipErrorNotReady) MOE_HIP(q);
-            (void)hipGetLastError();
+        if (q != hipSuccess && q != hipErrorNotReady) MOE_HIP(q);
+        (void)hipGetLastError();
+        bool landed = q == hipSuccess;
+        if (!landed && !rt->nonblocking) {
             MOE_HIP(hipStreamWaitEvent(sc, rt->ev_fill[layer], 0));
+            landed = true;
+        }
+        if (landed) {
+            for (const auto &fs : rt->pend_fill[layer]) row[fs.first] = fs.second;
+            rt->pend_fill[layer].clear();
+            rt->fill_pending[layer] = 0;
+            install = true;
         }
     }
+    int32_t *row_host = rt->h_rows + (size_t)layer * n;
+    if (install) std::memcpy(row_host, row, sizeof(int32_t) * n);
 
-    // Router; it publishes the routing and x to the host through the mailbox.
+    // Router; it publishes the routing and x to the host through the mailbox and
+    // installs the mirror row before the hit kernels read it.
     const int32_t seq = ++rt->seq;
     const float *wr = D.w_router + (size_t)layer * n * d;
-    MOE_HIP(moe::launch_router(x_dev, wr, 1, d, n, k, rt->d_idx, rt->d_w, sc, rt->mbox_dev, rt->h_x_dev, seq));
+    MOE_HIP(moe::launch_router(x_dev, wr, 1, d, n, k, rt->d_idx, rt->d_w, sc, rt->mbox_dev, rt->h_x_dev, seq,
+                               install ? rt->h_rows_dev + (size_t)layer * n : nullptr,
+                               rt->d_slotmap + (size_t)layer * n));
 
     // Hit experts on the device (slots from the device mirror of the table).
     moe::FfnParams p{};
@@ -383,6 +408,13 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
     for (int j = 0; j < k; ++j) nfill += fill[j] >= 0;
     if (covered && rt->cache->policy != MOE_POLICY_STATIC)
         for (int j = 0; j < k; ++j) rt->stats.fills_skipped += !hit[j] && fill[j] < 0;
+    // Where each expert runs: on the GPU iff this call's mirror row holds it (a cache hit
+    // whose post-fetch has landed); otherwise on the host.
+    for (int j = 0; j < k; ++j) {
+        const bool gpu = row[sel[j]] >= 0;
+        rt->stats.inflight_misses += hit[j] && !gpu;
+        hit[j] = gpu;
+    }
 
     int nmiss = 0, nhit = 0;
     const void *mslab[MOE_MAX_TOPK];
@@ -408,8 +440,20 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
     // previous token's kernels on this layer finished before this token's router.
     if (nfill) {
         uint8_t *set_base = static_cast<uint8_t *>(D.slot_pool) + (size_t)layer * D.ways * rt->slab_bytes;
+        auto &pf = rt->pend_fill[layer];
         for (int j = 0; j < k; ++j) {
             if (fill[j] < 0) continue;
+            // The evicted expert leaves the row at the next call, before any kernel could
+            // read its slot again; a victim still in flight is simply superseded.
+            if (evicted[j] >= 0) {
+                rt->pend_inval[layer].push_back(evicted[j]);
+                for (size_t q = 0; q < pf.size(); ++q)
+                    if (pf[q].first == evicted[j]) {
+                        pf.erase(pf.begin() + (ptrdiff_t)q);
+                        break;
+                    }
+            }
+            pf.emplace_back(sel[j], fill[j]);
             MOE_HIP(hipMemcpyAsync(set_base + (size_t)fill[j] * rt->slab_bytes,
                                    rt->host_slabs[(size_t)layer * n + sel[j]], rt->slab_payload,
                                    hipMemcpyHostToDevice, sw));
@@ -429,13 +473,8 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
     }
     MOE_HIP(moe::launch_ffn_reduce(p, nmiss ? rt->h_y_dev + (size_t)layer * d : nullptr, out_dev, sc));
 
-    // The mirror row is rewritten after this token's hit kernels have read it.
+    // The layer's copies are done when this event is; the next call installs them.
     if (nfill) {
-        int32_t *row = rt->h_slotmap + (size_t)layer * n;
-        std::memcpy(row, &rt->cache->where[(size_t)layer * n], sizeof(int32_t) * n);
-        MOE_HIP(hipEventRecord(rt->ev_hits, sc));
-        MOE_HIP(hipStreamWaitEvent(sw, rt->ev_hits, 0));
-        MOE_HIP(hipMemcpyAsync(rt->d_slotmap + (size_t)layer * n, row, sizeof(int32_t) * n, hipMemcpyHostToDevice, sw));
         MOE_HIP(hipEventRecord(rt->ev_fill[layer], sw));
         rt->fill_pending[layer] = 1;
         if (rt->fill_limit > 0) {
@@ -479,8 +518,30 @@ int moe_decode_step(moe_runtime *rt, const float *x_dev, float *out_dev, int32_t
 int moe_runtime_sync(moe_runtime *rt)
 {
     MOE_REQUIRE(rt, "moe_runtime_sync: null handle");
+    const int n = rt->desc.n;
+    bool any = false;
     for (int l = 0; l < rt->desc.n_layers; ++l)
-        if (rt->fill_pending[l]) MOE_HIP(hipEventSynchronize(rt->ev_fill[l]));
+        any = any || rt->fill_pending[l] || !rt->pend_inval[l].empty();
+    if (!any) return MOE_OK;
+    // Every copy has landed once the device is idle; install what the next calls would.
+    MOE_HIP(hipDeviceSynchronize());
+    for (int l = 0; l < rt->desc.n_layers; ++l) {
+        if (!rt->fill_pending[l] && rt->pend_inval[l].empty()) continue;
+        int32_t *row = &rt->dev_row[(size_t)l * n];
+        for (const int32_t v : rt->pend_inval[l]) row[v] = -1;
+        for (const auto &fs : rt->pend_fill[l]) row[fs.first] = fs.second;
+        rt->pend_inval[l].clear();
+        rt->pend_fill[l].clear();
+        rt->fill_pending[l] = 0;
+        MOE_HIP(hipMemcpy(rt->d_slotmap + (size_t)l * n, row, sizeof(int32_t) * n, hipMemcpyHostToDevice));
+    }
+    return MOE_OK;
+}
+
+int moe_runtime_set_nonblocking(moe_runtime *rt, int enable)
+{
+    MOE_REQUIRE(rt, "moe_runtime_set_nonblocking: null handle");
+    rt->nonblocking = enable != 0;
     return MOE_OK;
 }
 
@@ -488,7 +549,8 @@ int moe_runtime_device_slotmap(moe_runtime *rt, int layer, int32_t *slotmap_out)
 {
     MOE_REQUIRE(rt && slotmap_out, "moe_runtime_device_slotmap: null pointer");
     MOE_REQUIRE(layer >= 0 && layer < rt->desc.n_layers, "moe_runtime_device_slotmap: layer out of range");
-    if (rt->fill_pending[layer]) MOE_HIP(hipEventSynchronize(rt->ev_fill[layer]));
+    const int rc = moe_runtime_sync(rt);
+    if (rc != MOE_OK) return rc;
     MOE_HIP(hipMemcpy(slotmap_out, rt->d_slotmap + (size_t)layer * rt->desc.n, sizeof(int32_t) * rt->desc.n,
                       hipMemcpyDeviceToHost));
     return MOE_OK;

@@ -224,3 +224,44 @@ def test_runtime_bounded_postfetch(name, L, T, limit):
     assert st["fills_skipped"] == skipped
     assert st["fills"] + st["fills_skipped"] == st["expert_misses"]
     say("  worst max|err|/RMS", worst, "fills", st["fills"], "skipped", skipped)
+
+
+@pytest.mark.parametrize("name,L,T,limit", [("tiny", 3, 24, 0), ("mixtral", 2, 8, 0), ("mixtral", 2, 8, 2)])
+def test_runtime_nonblocking(name, L, T, limit):
+    """Non-blocking post-fetch: a layer call never waits for its set's copies; an expert
+    whose copy has not landed runs on the host. The cache table must still follow the
+    oracle bit for bit (read back before and after every call, replayed with the
+    insertions it shows), the GPU may only run table hits, every output must match the
+    oracle (no expert counted twice or lost), and after a sync the device mirror equals
+    the table."""
+    oracle.set_threads(min(16, os.cpu_count() or 1))
+    say("runtime non-blocking", name, L, T, limit)
+    world = World(name, L=L, T=T, threads=8)
+    world.rt.set_nonblocking(True)
+    world.rt.set_fill_limit(limit)
+    import torch
+    ref = olru.LRUCache(world.L, world.ways)
+    worst = 0.0
+    inflight = 0
+    for t in range(T):
+        for l in range(world.L):
+            before = world.cache.slotmap(l)
+            idx, w, gpu = world.rt.layer_forward(l, world.xd[t, l], world.out[t, l], world.streams)
+            after = world.cache.slotmap(l)
+            table_hits = [bool(before[e] >= 0) for e in idx]
+            inserted = [bool(after[e] >= 0) for e in idx]
+            slots, hits, fills, ev = ref.access(l, list(idx), inserted)
+            assert hits == table_hits, (t, l)
+            assert list(after) == ref.slotmap(l, world.n), (t, l)
+            assert all(h or not g for g, h in zip(gpu, table_hits)), (t, l)   # GPU runs table hits only
+            inflight += sum(1 for g, h in zip(gpu, table_hits) if h and not g)
+            torch.cuda.synchronize()
+            oidx, ow = router_parity(idx, w, world.X[l, t], world.wr[l], world.k)
+            o = world.oracle_out(l, t, oidx)
+            worst = max(worst, assert_close(world.out[t, l].cpu().numpy(), o, f"t={t} layer={l}"))
+    world.rt.sync()
+    for l in range(world.L):
+        assert list(world.rt.device_slotmap(l)) == ref.slotmap(l, world.n)
+    st = world.rt.stats()
+    assert st["inflight_misses"] == inflight
+    say("  worst max|err|/RMS", worst, "in-flight misses", inflight, "fills", st["fills"])
