@@ -35,6 +35,7 @@ typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 constexpr int kThreads = 256;
 constexpr int kBK = 64;         // K per stage
 constexpr int kLdsStride = kBK + 8;   // bf16 per LDS row (16-byte pad against bank conflicts)
+constexpr int kRowChunks = kBK / 8;  // 16-byte chunks of a token row per step
 constexpr int kXcds = 8;
 constexpr int kSpreadTokens = 64;   // below this many (token, expert) pairs per expert, spread items over XCDs
 constexpr int kMaxDownSplits = 4;
@@ -143,9 +144,10 @@ struct GemmArgs {
 // and every load instruction reads 64 contiguous bytes from each of 16 rows (with the
 // 32x32x16 shape it would be 32 bytes from 32 rows, which halves the rate HBM delivers).
 // Only the token tile (shared by the 8 waves) is staged in LDS, double-buffered.
-// Loads run kS K steps ahead in a ring of kS register sets; the K loop is unrolled by kS
-// so that every set is a fixed group of registers and each wait covers exactly the
-// oldest set. All loads are unconditional: token rows past the tile re-read row 0 (their
+// Loads run kS - 1 K steps ahead in a ring of kS register sets (kS = 4 in both launches
+// below: three steps, 96 KiB of weights per compute unit, in flight); the K loop is
+// unrolled by kS so that every set is a fixed group of registers and each wait covers
+// exactly the oldest set. All loads are unconditional: token rows past the tile re-read row 0 (their
 // outputs are dropped) and steps past the end re-read the last step.
 //
 // gate/up: a wave's two column blocks are 16 W1 rows and the same 16 W3 rows, so the gate
@@ -158,12 +160,72 @@ constexpr int kMBlocks = 12;                           // 16-token blocks per ti
 constexpr int kTileM = kMBlocks * 16;                  // 192 tokens
 constexpr int kKBlocks = kBK / 32;                     // MFMA K blocks per step
 
+// The K loop of k_moe_gemm for a tile of NMB 16-token blocks. NMB is a compile-time
+// constant so the MFMA sequence of a step has no branches: the compiler can then issue
+// the LDS reads of the token blocks ahead of the MFMAs that use them (with a run-time
+// block count every block was its own branch, and each MFMA pair waited for its own LDS
+// read). Blocks past the tile's last token are not computed.
+template <int kS, int kNB, int kAN, int kThr, int NMB>
+__device__ __forceinline__ void gemm_k_loop(uint16_t (*lds_a)[kTileM * kLdsStride], const uint16_t *const (&asrc)[kAN],
+                                            const uint16_t *const (&bsrc)[kNB], int nsteps,
+                                            floatx4_t (&acc)[kMBlocks][kNB])
+{
+    const int tid = threadIdx.x, lane = tid & 63;
+    u32x4_t ra[kS][kAN], rb[kS][kNB * kKBlocks];
+#define MOE_LOAD(set, step)                                                                           \
+    do {                                                                                              \
+        const int ko_ = min((step), nsteps - 1) * kBK;                                                \
+        _Pragma("unroll") for (int i = 0; i < kAN; ++i) ra[set][i] =                                \
+            *reinterpret_cast<const u32x4_t *>(asrc[i] + ko_);                                        \
+        _Pragma("unroll") for (int nb = 0; nb < kNB; ++nb)                                            \
+        _Pragma("unroll") for (int kb = 0; kb < kKBlocks; ++kb) rb[set][nb * kKBlocks + kb] =         \
+            *reinterpret_cast<const u32x4_t *>(bsrc[nb] + ko_ + 32 * kb);                             \
+    } while (0)
+#define MOE_STASH(set, buf)                                                                           \
+    do {                                                                                              \
+        _Pragma("unroll") for (int i = 0; i < kAN; ++i) {                                           \
+            const int c_ = tid + kThr * i;                                                       \
+            if (kTileM * kRowChunks % kThr == 0 || c_ < kTileM * kRowChunks)                          \
+                *reinterpret_cast<u32x4_t *>(&lds_a[buf][(c_ / kRowChunks) * kLdsStride + (c_ % kRowChunks) * 8]) = ra[set][i]; \
+        }                                                                                             \
+    } while (0)
+#define MOE_MMA(set, buf)                                                                             \
+    do {                                                                                              \
+        _Pragma("unroll") for (int kb = 0; kb < kKBlocks; ++kb) {                                     \
+            _Pragma("unroll") for (int m = 0; m < NMB; ++m) {                                         \
+                const bf16x8_t a_ = *reinterpret_cast<const bf16x8_t *>(                              \
+                    &lds_a[buf][(m * 16 + (lane & 15)) * kLdsStride + kb * 32 + 8 * (lane >> 4)]);     \
+                _Pragma("unroll") for (int nb = 0; nb < kNB; ++nb) acc[m][nb] =                       \
+                    __builtin_amdgcn_mfma_f32_16x16x32_bf16(                                          \
+                        a_, __builtin_bit_cast(bf16x8_t, rb[set][nb * kKBlocks + kb]), acc[m][nb], 0, 0, 0); \
+            }                                                                                         \
+        }                                                                                             \
+    } while (0)
+
+#pragma unroll
+    for (int p = 0; p < kS - 1; ++p) MOE_LOAD(p, p);
+    MOE_STASH(0, 0);
+    __syncthreads();
+    for (int s = 0; s < nsteps; s += kS) {
+#pragma unroll
+        for (int u = 0; u < kS; ++u) {
+            if (s + u >= nsteps) break;
+            MOE_LOAD((u + kS - 1) % kS, s + u + kS - 1);
+            MOE_MMA(u, (s + u) & 1);
+            MOE_STASH((u + 1) % kS, (s + u + 1) & 1);
+            __syncthreads();
+        }
+    }
+#undef MOE_LOAD
+#undef MOE_STASH
+#undef MOE_MMA
+}
+
 template <bool kGateUp, int kS, int kNB, int kWaves>
 __global__ __launch_bounds__(kWaves * 64) void k_moe_gemm(GemmArgs g)
 {
     constexpr int kThr = kWaves * 64;
-    constexpr int kAN = kTileM * 8 / kThr;             // token-tile 16-byte chunks per thread per step
-    static_assert(kTileM * 8 % kThr == 0, "token tile must split evenly over the threads");
+    constexpr int kAN = (kTileM * kRowChunks + kThr - 1) / kThr;   // token-tile 16-byte chunks per thread per step
     __shared__ uint16_t lds_a[2][kTileM * kLdsStride];
 
     const int per_expert = g.mtiles * g.ntiles * g.ksplit;
@@ -208,72 +270,33 @@ __global__ __launch_bounds__(kWaves * 64) void k_moe_gemm(GemmArgs g)
             bsrc[nb] = w + (size_t)2 * g.f * g.d + wrow * g.f + k0 + 8 * (lane >> 4);
         }
     }
-    // token-tile chunks staged by this thread: chunk c = tid + 512 i is row c / 8, 16-byte column c % 8
+    // token-tile chunks staged by this thread: chunk c = tid + kThr i is row c / kRowChunks, column
+    // c % kRowChunks (chunks past the tile, when the threads do not divide it, load row 0 and are not stored)
     const uint16_t *asrc[kAN];
 #pragma unroll
     for (int i = 0; i < kAN; ++i) {
         const int c = tid + kThr * i;
-        const int r = c >> 3, col = (c & 7) * 8;
+        const int r = c / kRowChunks, col = (c % kRowChunks) * 8;
         const int rr = r < rows ? r : 0;
         if (kGateUp) asrc[i] = g.a + (size_t)(g.perm[row0 + rr] / g.k) * g.d + k0 + col;
         else asrc[i] = g.a + (size_t)(row0 + rr) * g.f + k0 + col;
     }
 
-    u32x4_t ra[kS][kAN], rb[kS][kNB * kKBlocks];
     floatx4_t acc[kMBlocks][kNB];
 #pragma unroll
     for (int m = 0; m < kMBlocks; ++m)
 #pragma unroll
         for (int nb = 0; nb < kNB; ++nb) acc[m][nb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
-#define MOE_LOAD(set, step)                                                                           \
-    do {                                                                                              \
-        const int ko_ = min((step), nsteps - 1) * kBK;                                                \
-        _Pragma("unroll") for (int i = 0; i < kAN; ++i) ra[set][i] =                                \
-            *reinterpret_cast<const u32x4_t *>(asrc[i] + ko_);                                        \
-        _Pragma("unroll") for (int nb = 0; nb < kNB; ++nb)                                            \
-        _Pragma("unroll") for (int kb = 0; kb < kKBlocks; ++kb) rb[set][nb * kKBlocks + kb] =         \
-            *reinterpret_cast<const u32x4_t *>(bsrc[nb] + ko_ + 32 * kb);                             \
-    } while (0)
-#define MOE_STASH(set, buf)                                                                           \
-    do {                                                                                              \
-        _Pragma("unroll") for (int i = 0; i < kAN; ++i) {                                           \
-            const int c_ = tid + kThr * i;                                                       \
-            *reinterpret_cast<u32x4_t *>(&lds_a[buf][(c_ >> 3) * kLdsStride + (c_ & 7) * 8]) = ra[set][i]; \
-        }                                                                                             \
-    } while (0)
-#define MOE_MMA(set, buf)                                                                             \
-    do {                                                                                              \
-        _Pragma("unroll") for (int kb = 0; kb < kKBlocks; ++kb) {                                     \
-            _Pragma("unroll") for (int m = 0; m < kMBlocks; ++m) {                                    \
-                if (m < nmb) {                                                                        \
-                    const bf16x8_t a_ = *reinterpret_cast<const bf16x8_t *>(                          \
-                        &lds_a[buf][(m * 16 + (lane & 15)) * kLdsStride + kb * 32 + 8 * (lane >> 4)]); \
-                    _Pragma("unroll") for (int nb = 0; nb < kNB; ++nb) acc[m][nb] =                   \
-                        __builtin_amdgcn_mfma_f32_16x16x32_bf16(                                      \
-                            a_, __builtin_bit_cast(bf16x8_t, rb[set][nb * kKBlocks + kb]), acc[m][nb], 0, 0, 0); \
-                }                                                                                     \
-            }                                                                                         \
-        }                                                                                             \
-    } while (0)
-
-#pragma unroll
-    for (int p = 0; p < kS - 1; ++p) MOE_LOAD(p, p);
-    MOE_STASH(0, 0);
-    __syncthreads();
-    for (int s = 0; s < nsteps; s += kS) {
-#pragma unroll
-        for (int u = 0; u < kS; ++u) {
-            if (s + u >= nsteps) break;
-            MOE_LOAD((u + kS - 1) % kS, s + u + kS - 1);
-            MOE_MMA(u, (s + u) & 1);
-            MOE_STASH((u + 1) % kS, (s + u + 1) & 1);
-            __syncthreads();
-        }
+    // One copy of the K loop per token-block count, chosen once per work group.
+    switch (nmb) {
+#define MOE_NMB_CASE(N) \
+    case N: gemm_k_loop<kS, kNB, kAN, kThr, N>(lds_a, asrc, bsrc, nsteps, acc); break;
+        MOE_NMB_CASE(1) MOE_NMB_CASE(2) MOE_NMB_CASE(3) MOE_NMB_CASE(4) MOE_NMB_CASE(5) MOE_NMB_CASE(6)
+        MOE_NMB_CASE(7) MOE_NMB_CASE(8) MOE_NMB_CASE(9) MOE_NMB_CASE(10) MOE_NMB_CASE(11) MOE_NMB_CASE(12)
+#undef MOE_NMB_CASE
+    default: break;
     }
-#undef MOE_LOAD
-#undef MOE_STASH
-#undef MOE_MMA
 
     // Output element r of a 16x16 block sits at row 4*(lane/16) + r, column lane%16.
     const int P = g.off[g.n];
@@ -415,7 +438,7 @@ hipError_t launch_prefill(const PrefillPlan &P, const float *X, float *OUT, int3
     g.ntiles = P.f / (kGWaves * 16);
     g.ksplit = 1;
     g.per_xcd = groups * g.mtiles * g.ntiles * g.ksplit;
-    hipLaunchKernelGGL((k_moe_gemm<true, 2, 2, kGWaves>), dim3(grid_of(g)), dim3(kGWaves * 64), 0, s, g);
+    hipLaunchKernelGGL((k_moe_gemm<true, 4, 2, kGWaves>), dim3(grid_of(g)), dim3(kGWaves * 64), 0, s, g);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     // down: 256 (or 128) output rows per work group, K = f split in 4 (or 2) parts
