@@ -357,6 +357,32 @@ def measured_traffic(args):
     return rec["k_gate_up"]["hbm_bytes_per_launch"]
 
 
+def read_stream_yardstick(torch, moe, buf, launch_bytes):
+    """HBM read ceiling on this device: the library's plain nontemporal read stream over
+    (i) as many bytes as one average k_gate_up launch reads and (ii) a long read, both from
+    the device expert cache (event-timed on the launching stream, median of 20)."""
+    total = buf.numel() * buf.element_size()
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    out = {}
+    for name, nb in (("launch_size", launch_bytes), ("long", min(total, 8 << 30))):
+        nb = int(min(nb, total)) // 16 * 16
+        if nb <= 0:
+            continue
+        times = []
+        for it in range(23):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            moe.read_stream(buf, nb, sink)
+            e1.record()
+            e1.synchronize()
+            if it >= 3:
+                times.append(e0.elapsed_time(e1))
+        ms = sorted(times)[len(times) // 2]
+        out[name] = {"bytes": nb, "us": round(ms * 1e3, 2), "gbs": round(nb / (ms * 1e-3) / 1e9, 1),
+                     "frac": round(nb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    return out
+
+
 def bench_prefill(args, torch, moe, synth, wl):
     """One prompt of wl.T tokens through every layer, all experts resident in HBM
     (L x n slabs, layers visited in order so no slab is reused while cached)."""
@@ -582,6 +608,12 @@ def main():
         },
     }
     log(json.dumps(result["trace"]), json.dumps(result["hit_ffn"]))
+    if world["pool"] is not None and st["gate_up_launches"]:
+        ys = read_stream_yardstick(torch, moe, world["pool"], result["roofline"]["bytes_per_launch"])
+        if "launch_size" in ys:
+            ys["k_gate_up_frac_of_launch_size_stream"] = round(gu_gbs / ys["launch_size"]["gbs"], 4)
+        result["read_stream"] = ys
+        log(json.dumps(ys))
     result["host_expert_layer"] = {
         "what": f"host FFN of one layer's {k} experts (all missed), alone, by thread count",
         "by_threads": host_sweep(moe, wl, world)}

@@ -344,6 +344,22 @@ int moe_prefill_forward(const moe_prefill_desc *P, const float *X_dev, int T, fl
                         int32_t *idx_dev, float *w_dev, void *workspace, size_t workspace_bytes,
                         void *stream);
 
+/* ------------------------------------------------------------------------- */
+/* Measurement yardstick (not part of the method).                           */
+/* ------------------------------------------------------------------------- */
+/*
+ * Reads `bytes` bytes at `buf` (device, 16-byte aligned; bytes a multiple of 16) with
+ * 16-byte nontemporal loads, 64 lanes covering 1 KiB per load (the access pattern of
+ * the decode weight kernels). The rate at which it runs is the practical HBM read
+ * ceiling that the weight-streaming kernels are compared with. `sink` (device, 4 bytes,
+ * caller-owned) receives a word only if a lane's XOR fold of what it read equals a
+ * fixed constant, which keeps the loads from being removed. grid = work groups of 256
+ * threads (0: eight per compute unit). Launched on `stream`; the caller times it.
+ * MOE_EINVAL on a null or misaligned pointer, bytes % 16 != 0 or grid < 0; bytes == 0
+ * launches nothing.
+ */
+int moe_read_stream(const void *buf, size_t bytes, uint32_t *sink, int grid, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

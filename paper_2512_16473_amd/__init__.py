@@ -21,7 +21,7 @@ _lib = _abi.load()
 
 __all__ = [
     "MoeError", "lib", "slab_bytes", "router_topk", "Cache", "ffn_workspace_bytes", "expert_ffn_hits",
-    "combine", "PinnedBuffer", "HostPool", "Runtime", "prefill_workspace_bytes", "prefill_forward",
+    "combine", "PinnedBuffer", "HostPool", "Runtime", "prefill_workspace_bytes", "prefill_forward", "read_stream",
 ]
 
 
@@ -319,3 +319,13 @@ def prefill_forward(X, w_router, expert_pool, d, f, n, k, OUT, workspace, idx=No
         ctypes.byref(P), _ptr(X), T, _ptr(OUT), _ptr(idx), _ptr(w), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream)))
     return OUT
+
+
+# --------------------------------------------------------------------------- yardstick
+def read_stream(buf, nbytes, sink, grid=0, stream=None):
+    """Plain nontemporal read of nbytes of the device tensor buf (the HBM read ceiling
+    used as a yardstick for the weight-streaming kernels); sink is a device tensor of at
+    least 4 bytes. Launched on `stream`; the caller times it."""
+    if nbytes > buf.numel() * buf.element_size():
+        raise ValueError(f"read_stream: {nbytes} bytes exceed the buffer")
+    _check("moe_read_stream", _lib.moe_read_stream(_ptr(buf), nbytes, _ptr(sink), grid, _stream(stream)))

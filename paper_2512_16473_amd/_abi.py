@@ -86,6 +86,7 @@ SIGNATURES = [
     ("moe_prefill_workspace_bytes", c_size_t, [ctypes.POINTER(PrefillDesc), c_int]),
     ("moe_prefill_forward", c_int, [ctypes.POINTER(PrefillDesc), c_void_p, c_int, c_void_p, c_void_p, c_void_p,
                                     c_void_p, c_size_t, c_void_p]),
+    ("moe_read_stream", c_int, [c_void_p, c_size_t, c_void_p, c_int, c_void_p]),
 ]
 
 

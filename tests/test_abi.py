@@ -55,6 +55,12 @@ def test_argument_errors_do_not_touch_the_device():
     assert lib.moe_expert_ffn_hits(None, None, 4, None, None, 17, 64, 64, None, None, 0, None) == _abi.MOE_EINVAL
     assert lib.moe_combine(None, None, None, 16, None, None) == _abi.MOE_EINVAL
     assert lib.moe_runtime_create(None, None) == _abi.MOE_EINVAL
+    # read-stream yardstick: size, grid and pointers checked before any HIP call
+    assert lib.moe_read_stream(None, 24, None, 0, None) == _abi.MOE_EINVAL
+    assert b"multiple of 16" in lib.moe_last_error()
+    assert lib.moe_read_stream(None, 32, None, -1, None) == _abi.MOE_EINVAL
+    assert lib.moe_read_stream(None, 32, None, 0, None) == _abi.MOE_EINVAL
+    assert lib.moe_read_stream(None, 0, None, 0, None) == _abi.MOE_OK   # nothing to read: no-op
 
 
 def test_cache_create_validation():
