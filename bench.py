@@ -137,13 +137,54 @@ def cpu_baseline(wl, world, seed, budget_s, t_first):
         if elapsed >= budget_s:
             break
     per_token_layer = elapsed / done
+    # the same token-layers again on one thread, for a shorter budget
+    oracle.set_threads(1)
+    done1, elapsed1 = 0, 0.0
+    try:
+        for (l, t) in order[:done]:
+            slabs = [hosts[l % H].array[e * stride:e * stride + 3 * d * f * 2].view(np.uint16) for e in range(n)]
+            sh = None
+            if shared_np is not None:
+                sh = shared_np[l * sstride: l * sstride + 3 * d * wl.f_shared * 2].view(np.uint16)
+            t0 = time.perf_counter()
+            oracle.moe_token(X[l, t], wr[l], slabs, k, f, shared_slab=sh, f_shared=wl.f_shared)
+            elapsed1 += time.perf_counter() - t0
+            done1 += 1
+            if elapsed1 >= budget_s / 4:
+                break
+    finally:
+        oracle.set_threads(threads)
     return {
         "value": 1.0 / (per_token_layer * L), "unit": "tokens/s", "cores": threads, "kind": "oracle",
         "sample": (f"{done} token-layers (layers {min(layers_used)}-{max(layers_used)}, consecutive tokens from "
                    f"step {t_first}) through router + top-{k} SwiGLU experts + combine + LRU, "
                    f"{elapsed:.1f}s; scaled to {L} layers per token"),
         "ms_per_token_layer": per_token_layer * 1e3,
+        "one_thread": {"tokens_per_s": 1.0 / (elapsed1 / done1 * L), "ms_per_token_layer": elapsed1 / done1 * 1e3,
+                       "sample": f"the first {done1} of those token-layers, {elapsed1:.1f}s"},
+        "host": host_info(),
     }
+
+
+def host_info():
+    """What the host that ran the oracle is: logical CPUs, the ones this process may use,
+    the CPU model and whether it has AVX-512 (and its bf16 extension)."""
+    model, flags = "unknown", set()
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name") and model == "unknown":
+                    model = line.split(":", 1)[1].strip()
+                elif line.startswith("flags") and not flags:
+                    flags = set(line.split(":", 1)[1].split())
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = None
+    return {"nproc": os.cpu_count(), "usable_cpus": usable, "cpu_model": model,
+            "avx512f": "avx512f" in flags, "avx512_bf16": "avx512_bf16" in flags}
 
 
 def host_sweep(moe, wl, world, threads_list=(1, 2, 4, 8, 16)):
