@@ -265,3 +265,48 @@ def test_runtime_nonblocking(name, L, T, limit):
     st = world.rt.stats()
     assert st["inflight_misses"] == inflight
     say("  worst max|err|/RMS", worst, "in-flight misses", inflight, "fills", st["fills"])
+
+
+@pytest.mark.parametrize("nonblocking", [False, True])
+def test_runtime_delayed_copies(nonblocking):
+    """Post-fetch copies held back on purpose: before every token a bounded spin kernel
+    (about 10 ms) is queued on the copy stream, so each token's post-fetches land late.
+    Parity mode must then make the compute stream wait for them (trace and outputs equal
+    to the oracle, as without the delay); non-blocking mode must run the experts whose
+    copies are still in flight on the host (some of them do, every output still
+    matches the oracle)."""
+    torch = torch_cuda()
+    oracle.set_threads(min(16, os.cpu_count() or 1))
+    say("runtime delayed copies, non-blocking" if nonblocking else "runtime delayed copies, parity")
+    world = World("tiny", L=3, T=24, threads=4)
+    world.rt.set_nonblocking(nonblocking)
+    ref = olru.LRUCache(world.L, world.ways)
+    worst, inflight = 0.0, 0
+    for t in range(world.T):
+        with torch.cuda.stream(world.streams[2]):
+            torch.cuda._sleep(20_000_000)
+        for l in range(world.L):
+            before = world.cache.slotmap(l)
+            idx, w, gpu = world.rt.layer_forward(l, world.xd[t, l], world.out[t, l], world.streams)
+            after = world.cache.slotmap(l)
+            table_hits = [bool(before[e] >= 0) for e in idx]
+            slots, hits, fills, ev = ref.access(l, list(idx), [bool(after[e] >= 0) for e in idx])
+            assert hits == table_hits, (t, l)
+            assert list(after) == ref.slotmap(l, world.n), (t, l)
+            if nonblocking:
+                assert all(h or not g for g, h in zip(gpu, table_hits)), (t, l)
+                inflight += sum(1 for g, h in zip(gpu, table_hits) if h and not g)
+            else:
+                assert list(gpu) == table_hits, (t, l)       # parity: every table hit runs on the GPU
+            world.streams[0].synchronize()    # the output only: the copy stream keeps running
+            oidx, ow = router_parity(idx, w, world.X[l, t], world.wr[l], world.k)
+            worst = max(worst, assert_close(world.out[t, l].cpu().numpy(), world.oracle_out(l, t, oidx),
+                                            f"t={t} layer={l}"))
+    world.rt.sync()
+    for l in range(world.L):
+        assert list(world.rt.device_slotmap(l)) == ref.slotmap(l, world.n)
+    st = world.rt.stats()
+    assert st["inflight_misses"] == inflight
+    if nonblocking:
+        assert inflight > 0
+    say("  worst max|err|/RMS", worst, "in-flight misses", inflight, "fills", st["fills"])
