@@ -250,6 +250,10 @@ void moe_runtime_destroy(moe_runtime *rt);
  * (Section III-C keeps them apart). The call returns after the host part (cache
  * update, miss FFN) is done and the device work is enqueued. Post-fetched experts
  * become usable from the next token at this layer; that next use waits for the copy.
+ * Calls on one runtime must not overlap (one calling thread at a time).
+ * Errors: MOE_EINVAL for bad arguments, with nothing changed. MOE_EHIP (a HIP failure,
+ * or routing not published within 60 s) can come after this call's cache update and
+ * copies were applied in part; the runtime is then unusable and must be destroyed.
  */
 int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out_dev,
                       int32_t *idx_host, float *w_host, uint8_t *hit_host,

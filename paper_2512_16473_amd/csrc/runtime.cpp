@@ -7,19 +7,19 @@
 //           (post-fetch), on a stream of its own (Section III-C keeps weight copies
 //           off the stream that carries activations).
 //
-// Device side, in stream order on the compute stream: [wait for the previous
-// post-fetch into this layer's set, if still running] router -> gate/up/SiLU ->
-// down -> reduce+combine, with no other commands between the kernels. The hit
-// kernels resolve expert -> slot on the device from a mirror of the host slot
-// table, so they never wait for the host. The router kernel itself hands the
-// routing and the hidden state to the host: it writes them into coherent pinned
-// memory followed by a sequence number, which the host polls (the activation
-// exchange never queues behind weight copies). The host then updates the LRU table,
-// starts the post-fetch copies, runs the misses on its thread pool into coherent
-// pinned memory that the reduce kernel reads directly, and enqueues the reduce.
-// The updated mirror row lands on the copy stream after this token's hit kernels;
-// the next token's use of this layer waits on that copy, so the hit/miss sequence
-// does not depend on timing.
+// Device side, in stream order on the compute stream: [parity mode: wait for this
+// layer's earlier post-fetch, if still running] router -> gate/up/SiLU -> down ->
+// reduce+combine, with no other commands between the kernels. The router kernel installs
+// the layer's row of the device expert->slot mirror (copied from coherent pinned memory
+// that holds the host's record of landed copies) before the hit kernels read it, and it
+// hands the routing and the hidden state to the host: it writes them into coherent
+// pinned memory followed by a sequence number, which the host polls (the activation
+// exchange never queues behind weight copies). The host then updates the cache table,
+// starts the post-fetch copies on the copy stream, runs the misses on its thread pool
+// into coherent pinned memory that the reduce kernel reads directly, and enqueues the
+// reduce. A post-fetched expert joins the mirror at a later call on its layer once its
+// copy has landed: parity mode waits for the copy, so the hit/miss sequence does not
+// depend on timing; non-blocking mode runs the expert on the host until then.
 #include <immintrin.h>
 
 #include <algorithm>
