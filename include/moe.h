@@ -147,6 +147,21 @@ int moe_cache_update_masked(moe_cache *c, int layer, const int32_t *experts, int
                             const uint8_t *insert, int32_t *fill_slot_out, int32_t *evicted_out);
 /* Expert -> slot table of one layer: host [n], -1 for experts not cached. */
 int moe_cache_slotmap(const moe_cache *c, int layer, int32_t *slotmap_out);
+/*
+ * Checkpoint and resume of the cache state (every set's slot contents, their recency
+ * stamps and the set clocks), so a stopped decode can continue with the same hit/miss
+ * sequence. moe_cache_state_bytes gives the size of a state (0 for NULL). moe_cache_save
+ * writes it into host memory `buf` of `bytes` >= that size. moe_cache_restore loads a
+ * saved state into a cache created with the same geometry, policy and static content;
+ * `bytes` must equal the state size. It returns MOE_EINVAL, leaving the cache unchanged,
+ * for another geometry or policy, or an inconsistent state: an expert id out of range or
+ * in two slots of a set, a resident slot stamped 0, after its set's clock or with
+ * another slot's stamp, a static set that differs from its content. A runtime created
+ * over the restored cache fills the slots it holds (moe_runtime_create).
+ */
+size_t moe_cache_state_bytes(const moe_cache *c);
+int moe_cache_save(const moe_cache *c, void *buf, size_t bytes);
+int moe_cache_restore(moe_cache *c, const void *buf, size_t bytes);
 
 /* ------------------------------------------------------------------------- */
 /* Cache-hit expert FFN on the GPU (Section III-A step 2(a)).                 */

@@ -139,6 +139,18 @@ class Cache:
         _check("moe_cache_slotmap", _lib.moe_cache_slotmap(self.handle, layer, _np_ptr(m, ctypes.c_int32)))
         return m
 
+    def save(self) -> bytes:
+        """The cache state (slots, recency stamps, set clocks) as bytes."""
+        nb = int(_lib.moe_cache_state_bytes(self.handle))
+        buf = ctypes.create_string_buffer(nb)
+        _check("moe_cache_save", _lib.moe_cache_save(self.handle, buf, nb))
+        return buf.raw
+
+    def restore(self, state: bytes):
+        """Load a state saved from a cache of the same geometry, policy and content."""
+        buf = ctypes.create_string_buffer(bytes(state), len(state))
+        _check("moe_cache_restore", _lib.moe_cache_restore(self.handle, buf, len(state)))
+
 
 def cache_geometry(budget_bytes, expert_bytes, ways, n_layers):
     """(slots S, covered layers min(N, n_layers)) for a memory budget (Section III-B)."""

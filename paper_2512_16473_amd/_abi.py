@@ -59,6 +59,9 @@ SIGNATURES = [
     ("moe_cache_update", c_int, [c_void_p, c_int, c_i32p, c_int, c_i32p, c_i32p]),
     ("moe_cache_update_masked", c_int, [c_void_p, c_int, c_i32p, c_int, c_u8p, c_i32p, c_i32p]),
     ("moe_cache_slotmap", c_int, [c_void_p, c_int, c_i32p]),
+    ("moe_cache_state_bytes", c_size_t, [c_void_p]),
+    ("moe_cache_save", c_int, [c_void_p, c_void_p, c_size_t]),
+    ("moe_cache_restore", c_int, [c_void_p, c_void_p, c_size_t]),
     ("moe_ffn_workspace_bytes", c_size_t, [c_int, c_int, c_int]),
     ("moe_expert_ffn_hits", c_int, [c_void_p, c_void_p, c_int, c_void_p, c_void_p, c_int, c_int, c_int,
                                     c_void_p, c_void_p, c_size_t, c_void_p]),

@@ -223,6 +223,96 @@ int moe_cache_update_masked(moe_cache *ch, int layer, const int32_t *experts, in
     return MOE_OK;
 }
 
+// Checkpoint layout (host byte order): a header of 7 int32 (magic, version, layers, n,
+// ways, top_k, policy), then slot experts int32 [layers][ways], slot stamps uint64
+// [layers][ways] and set clocks uint64 [layers]. The expert -> slot map is rebuilt.
+namespace {
+constexpr int32_t kStateMagic = 0x43454f4d;   // "MOEC"
+constexpr int32_t kStateVersion = 1;
+constexpr size_t kStateHeader = 7 * sizeof(int32_t);
+
+size_t state_bytes(const Cache *c)
+{
+    const size_t slots = (size_t)c->layers * c->ways;
+    return kStateHeader + slots * sizeof(int32_t) + slots * sizeof(uint64_t) + (size_t)c->layers * sizeof(uint64_t);
+}
+}  // namespace
+
+size_t moe_cache_state_bytes(const moe_cache *ch)
+{
+    const Cache *c = reinterpret_cast<const Cache *>(ch);
+    return c ? state_bytes(c) : 0;
+}
+
+int moe_cache_save(const moe_cache *ch, void *buf, size_t bytes)
+{
+    const Cache *c = reinterpret_cast<const Cache *>(ch);
+    MOE_REQUIRE(c && buf, "moe_cache_save: null pointer");
+    MOE_REQUIRE(bytes >= state_bytes(c), "moe_cache_save: buffer of %zu bytes, %zu needed", bytes, state_bytes(c));
+    const int32_t head[7] = {kStateMagic, kStateVersion, c->layers, c->n, c->ways, c->top_k, c->policy};
+    uint8_t *o = static_cast<uint8_t *>(buf);
+    std::memcpy(o, head, kStateHeader);
+    o += kStateHeader;
+    const size_t slots = (size_t)c->layers * c->ways;
+    std::memcpy(o, c->slot_expert.data(), slots * sizeof(int32_t));
+    o += slots * sizeof(int32_t);
+    std::memcpy(o, c->slot_used.data(), slots * sizeof(uint64_t));
+    o += slots * sizeof(uint64_t);
+    std::memcpy(o, c->tick.data(), (size_t)c->layers * sizeof(uint64_t));
+    return MOE_OK;
+}
+
+int moe_cache_restore(moe_cache *ch, const void *buf, size_t bytes)
+{
+    MOE_GUARD_BEGIN
+    Cache *c = reinterpret_cast<Cache *>(ch);
+    MOE_REQUIRE(c && buf, "moe_cache_restore: null pointer");
+    MOE_REQUIRE(bytes == state_bytes(c), "moe_cache_restore: %zu bytes, a state of this cache has %zu", bytes,
+                state_bytes(c));
+    const uint8_t *in = static_cast<const uint8_t *>(buf);
+    int32_t head[7];
+    std::memcpy(head, in, kStateHeader);
+    MOE_REQUIRE(head[0] == kStateMagic && head[1] == kStateVersion, "moe_cache_restore: not a cache state");
+    MOE_REQUIRE(head[2] == c->layers && head[3] == c->n && head[4] == c->ways && head[5] == c->top_k &&
+                    head[6] == c->policy,
+                "moe_cache_restore: state of a cache with another geometry or policy");
+    const size_t slots = (size_t)c->layers * c->ways;
+    std::vector<int32_t> sx(slots);
+    std::vector<uint64_t> su(slots), clk((size_t)c->layers);
+    std::memcpy(sx.data(), in + kStateHeader, slots * sizeof(int32_t));
+    std::memcpy(su.data(), in + kStateHeader + slots * sizeof(int32_t), slots * sizeof(uint64_t));
+    std::memcpy(clk.data(), in + kStateHeader + slots * (sizeof(int32_t) + sizeof(uint64_t)),
+                (size_t)c->layers * sizeof(uint64_t));
+    std::vector<int32_t> where((size_t)c->layers * c->n, -1);
+    for (int l = 0; l < c->layers; ++l)
+        for (int q = 0; q < c->ways; ++q) {
+            const size_t i = (size_t)l * c->ways + q;
+            const int32_t e = sx[i];
+            MOE_REQUIRE(e >= -1 && e < c->n, "moe_cache_restore: expert %d in layer %d out of range", e, l);
+            if (c->policy == MOE_POLICY_STATIC) {
+                MOE_REQUIRE(e == c->initial[i] && su[i] == 0 && clk[l] == 0,
+                            "moe_cache_restore: layer %d differs from the static content", l);
+            } else if (e >= 0) {
+                // a resident expert was stamped when the set's clock reached its stamp
+                MOE_REQUIRE(su[i] >= 1 && su[i] <= clk[l], "moe_cache_restore: slot stamp after the clock (layer %d)",
+                            l);
+                for (int r = 0; r < q; ++r)
+                    MOE_REQUIRE(sx[(size_t)l * c->ways + r] < 0 || su[(size_t)l * c->ways + r] != su[i],
+                                "moe_cache_restore: two slots of layer %d with one stamp", l);
+            }
+            if (e >= 0) {
+                MOE_REQUIRE(where[(size_t)l * c->n + e] < 0, "moe_cache_restore: expert %d twice in layer %d", e, l);
+                where[(size_t)l * c->n + e] = q;
+            }
+        }
+    c->slot_expert.swap(sx);
+    c->slot_used.swap(su);
+    c->tick.swap(clk);
+    c->where.swap(where);
+    return MOE_OK;
+    MOE_GUARD_END
+}
+
 int moe_cache_slotmap(const moe_cache *ch, int layer, int32_t *slotmap_out)
 {
     const Cache *c = reinterpret_cast<const Cache *>(ch);

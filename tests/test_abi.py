@@ -179,6 +179,90 @@ def test_library_masked_insertion_vs_oracle(policy):
             assert list(c.slotmap(layer)) == ref.slotmap(layer, n)
 
 
+@pytest.mark.parametrize("policy", ["lru", "fifo", "static"])
+def test_cache_checkpoint_resume(policy):
+    """A cache saved mid-trace and restored into a new cache of the same geometry goes on
+    exactly like the original and like the oracle's uninterrupted cache (plain and masked
+    insertion), and restoring returns the table it was saved from."""
+    rng = random.Random(17 + sum(map(ord, policy)))
+    n, k, ways, L = 8, 2, 4, 3
+    content = [rng.sample(range(n), ways) for _ in range(L)] if policy == "static" else None
+    a = moe.Cache(L, n, ways, k, policy=policy, static_content=content)
+    ref = olru.LRUCache(L, ways, policy=policy, static_content=content)
+
+    def step(caches, layer, sel, ins):
+        r = ref.access(layer, sel, ins)
+        for c in caches:
+            slots, hits = c.lookup(layer, sel)
+            fill, ev = c.update_masked(layer, sel, ins)
+            assert (list(slots), list(hits), list(fill), list(ev)) == r
+            assert list(c.slotmap(layer)) == ref.slotmap(layer, n)
+
+    for t in range(40):
+        for layer in range(L):
+            sel = rng.sample(range(n), k)
+            step([a], layer, sel, [rng.random() < 0.8 for _ in sel])
+    state = a.save()
+    assert len(state) == 28 + L * ways * 12 + L * 8
+    b = moe.Cache(L, n, ways, k, policy=policy, static_content=content)
+    b.restore(state)
+    assert b.save() == state
+    for layer in range(L):
+        assert list(b.slotmap(layer)) == list(a.slotmap(layer))
+    for t in range(40):
+        for layer in range(L):
+            sel = rng.sample(range(n), k)
+            step([a, b], layer, sel, [rng.random() < 0.8 for _ in sel])
+
+
+def test_cache_restore_rejects_bad_states():
+    """A state of another geometry or policy, a truncated or foreign buffer, and
+    inconsistent contents are refused with EINVAL and leave the cache as it was."""
+    import struct
+    n, k, ways, L = 8, 2, 4, 2
+    src = moe.Cache(L, n, ways, k)
+    for sel in ([0, 1], [2, 3], [4, 1], [5, 6]):
+        src.update(0, sel)
+    good = bytearray(src.save())
+    dst = moe.Cache(L, n, ways, k)
+    dst.update(1, [7, 6])
+    before = dst.save()
+    head, sx0, su0, ck0 = 28, 28, 28 + L * ways * 4, 28 + L * ways * 12
+
+    def patched(off, fmt, value):
+        b = bytearray(good)
+        struct.pack_into(fmt, b, off, value)
+        return bytes(b)
+
+    bad = {
+        "truncated": bytes(good[:-1]),
+        "foreign": b"x" * len(good),
+        "other policy": patched(24, "<i", 1),
+        "expert out of range": patched(sx0, "<i", n),
+        "expert twice": patched(sx0 + 4, "<i", struct.unpack_from("<i", good, sx0)[0]),
+        "stamp after clock": patched(su0, "<Q", struct.unpack_from("<Q", good, ck0)[0] + 1),
+        "stamp 0 on a resident slot": patched(su0, "<Q", 0),
+        "two slots one stamp": patched(su0 + 8, "<Q", struct.unpack_from("<Q", good, su0)[0]),
+    }
+    for what, state in bad.items():
+        with pytest.raises(moe.MoeError):
+            dst.restore(state)
+        assert dst.save() == before, what
+    with pytest.raises(moe.MoeError):
+        moe.Cache(L, n, ways + 1, k).restore(bytes(good))          # another geometry
+    with pytest.raises(moe.MoeError):
+        moe.Cache(L, n, ways, k, policy="static",
+                  static_content=[[0, 1, 2, 3]] * L).restore(bytes(good))
+    st = moe.Cache(1, n, 2, 2, policy="static", static_content=[[3, 5]]).save()
+    with pytest.raises(moe.MoeError):    # a static set whose content differs
+        moe.Cache(1, n, 2, 2, policy="static", static_content=[[5, 3]]).restore(st)
+    lib = _abi.load()
+    assert lib.moe_cache_state_bytes(None) == 0
+    assert lib.moe_cache_save(None, None, 0) == _abi.MOE_EINVAL
+    buf = ctypes.create_string_buffer(len(good) - 1)
+    assert lib.moe_cache_save(src.handle, buf, len(good) - 1) == _abi.MOE_EINVAL
+
+
 def test_static_policy_validation():
     with pytest.raises(moe.MoeError):
         moe.Cache(1, 8, 2, 2, policy="static", static_content=[[1, 1]])      # duplicate

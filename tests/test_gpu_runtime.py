@@ -310,3 +310,39 @@ def test_runtime_delayed_copies(nonblocking):
     if nonblocking:
         assert inflight > 0
     say("  worst max|err|/RMS", worst, "in-flight misses", inflight, "fills", st["fills"])
+
+
+def test_runtime_resume_from_checkpoint():
+    """Stop a decode half way, save the cache state, drop the runtime and clear the
+    device slot pool (as a new process would start), restore the state into a new cache
+    and runtime: the runtime refills the held slots from the host, and the continued
+    trace and outputs equal the oracle's uninterrupted run."""
+    torch = torch_cuda()
+    import paper_2512_16473_amd as moe
+    say("runtime resume from a cache checkpoint")
+    world = World("tiny", L=3, T=24, threads=4)
+    half = world.T // 2
+    idx = np.empty((world.T, world.L, world.k), np.int32)
+    w = np.empty((world.T, world.L, world.k), np.float32)
+    hit = np.empty((world.T, world.L, world.k), np.uint8)
+    for t in range(half):
+        world.rt.decode_step(world.xd[t], world.out[t], world.streams, idx[t], w[t], hit[t])
+    torch.cuda.synchronize()
+    world.rt.sync()
+    state = world.cache.save()
+    world.rt.close()
+    world.cache.close()
+    world.pool.zero_()
+    torch.cuda.synchronize()
+    cache = moe.Cache(world.L, world.n, world.ways, world.k)
+    cache.restore(state)
+    rt = moe.Runtime(world.d, world.f, world.n, world.k, world.ways, world.L, torch.from_numpy(world.wr).cuda(),
+                     world.pool, world.host_addrs, cache, world.hpool)
+    world.cache, world.rt = cache, rt
+    for t in range(half, world.T):
+        rt.decode_step(world.xd[t], world.out[t], world.streams, idx[t], w[t], hit[t])
+    torch.cuda.synchronize()
+    rt.sync()
+    out = world.out.cpu().numpy()
+    worst = _check_trace(world, idx, w, hit.astype(bool), out, world.T, set(range(world.L)), lambda t, l: True)
+    say("  worst max|err|/RMS", worst)
