@@ -7,7 +7,8 @@
 // against each set's own invariants (at most `ways` experts, no duplicates, slot ids in
 // range, the selected experts resident after an LRU/FIFO step unless their insertion
 // was masked, the static content never changing, lookup agreeing with the slot table
-// and with the previous step's fills); rejected calls leave the state unchanged; reset;
+// and with the previous step's fills); checkpoint round trips and refused damaged states;
+// rejected calls leave the state unchanged; reset;
 // geometry; the host expert FFN identical (bit for bit) on 1, 2 and 5 threads, and zero
 // for zero experts.
 #include <hip/hip_runtime_api.h>
@@ -128,6 +129,27 @@ static void trace_policy(int policy, bool masked, unsigned seed)
         // the other layers are untouched
         if (policy == MOE_POLICY_STATIC)
             for (int j = 0; j < ways; ++j) CHECK(after[content[l * ways + j]] == j, "static content changed");
+    }
+    // checkpoint round trip, and a damaged or truncated state refused
+    {
+        const size_t nb = moe_cache_state_bytes(c);
+        std::vector<uint8_t> st(nb), st2(nb);
+        CHECK(moe_cache_save(c, st.data(), nb) == MOE_OK, "save");
+        moe_cache *d = nullptr;
+        CHECK(moe_cache_create_policy(L, n, ways, k, policy, content.empty() ? nullptr : content.data(), &d) ==
+                  MOE_OK, "create for restore");
+        CHECK(moe_cache_restore(d, st.data(), nb) == MOE_OK, "restore");
+        CHECK(moe_cache_save(d, st2.data(), nb) == MOE_OK && st == st2, "restored state differs");
+        for (int l = 0; l < L; ++l) CHECK(slotmap(d, l, n) == slotmap(c, l, n), "restored table differs");
+        CHECK(moe_cache_restore(d, st.data(), nb - 1) == MOE_EINVAL, "truncated state accepted");
+        std::vector<uint8_t> bad = st;
+        bad[28] = 0xff;   // first slot's expert id becomes negative and out of range
+        bad[29] = 0xff;
+        bad[30] = 0xff;
+        bad[31] = 0x80;
+        CHECK(moe_cache_restore(d, bad.data(), nb) == MOE_EINVAL, "damaged state accepted");
+        CHECK(moe_cache_save(d, st2.data(), nb) == MOE_OK && st == st2, "refused restore changed the cache");
+        moe_cache_destroy(d);
     }
     // rejected calls change nothing
     const std::vector<int32_t> keep = slotmap(c, 0, n);
