@@ -322,8 +322,9 @@ def pcie_study(args, torch, moe, synth, wl):
 def small_batch_study(args, torch, moe, synth, wl):
     """Multi-token decode with every expert resident (T = 1..64 tokens per step): the
     grouped-GEMM path (prefill kernels at small T) against T single-token passes of the
-    GEMV hit path, per MoE layer. Not in the paper; it locates the GEMV -> GEMM
-    crossover between the decode and prefill kernels."""
+    GEMV hit path and, for T <= 8, the multi-token GEMV path (each selected slab read once
+    for all its tokens), per MoE layer. Not in the paper; it locates the crossovers
+    between the decode and prefill kernels."""
     import numpy as np
     d, f, n, k = wl.d, wl.f, wl.n, wl.k
     L = 4                                   # distinct layers so weights are not reused from cache
@@ -344,6 +345,9 @@ def small_batch_study(args, torch, moe, synth, wl):
     idx = torch.empty((Tmax, k), dtype=torch.int32, device="cuda")
     wts = torch.empty((Tmax, k), dtype=torch.float32, device="cuda")
     y = torch.empty(d, device="cuda")
+    tmax_tok = min(moe.MAX_TOKENS, 131072 // (4 * d))
+    tws = torch.empty(moe.ffn_tokens_workspace_bytes(tmax_tok, k, d, f), dtype=torch.uint8, device="cuda")
+    ytok = torch.empty((tmax_tok, d), device="cuda")
 
     def time_it(fn, reps=5):
         fn()
@@ -368,15 +372,25 @@ def small_batch_study(args, torch, moe, synth, wl):
                 for t in range(T):
                     moe.expert_ffn_hits(X[t], pool[l * n * stride:(l + 1) * n * stride], n, idx[t], wts[t], d, f, y,
                                         fws)
+        def tokens():
+            for l in range(L):
+                moe.router_topk(X[:T], wr[l], k, idx_out=idx[:T], w_out=wts[:T])
+                moe.expert_ffn_tokens(X[:T], pool[l * n * stride:(l + 1) * n * stride], n, idx[:T], wts[:T], d, f,
+                                      ytok[:T], tws)
         g_us = time_it(grouped) / L
         v_us = time_it(gemv, reps=2 if T >= 16 else 5) / L
+        t_us = time_it(tokens) / L if T <= tmax_tok else None
         touched = int(np.unique(idx[:T].cpu().numpy()).size)
         rows.append({"T": T, "grouped_us_per_layer": round(g_us, 1), "gemv_us_per_layer": round(v_us, 1),
+                     "tokens_us_per_layer": None if t_us is None else round(t_us, 1),
                      "experts_touched": touched,
-                     "grouped_weight_GBs": round(touched * 3 * d * f * 2 / (g_us * 1e-6) / 1e9, 1)})
+                     "grouped_weight_GBs": round(touched * 3 * d * f * 2 / (g_us * 1e-6) / 1e9, 1),
+                     "tokens_weight_GBs": None if t_us is None else
+                     round(touched * 3 * d * f * 2 / (t_us * 1e-6) / 1e9, 1)})
         log(json.dumps(rows[-1]))
     return {
-        "metric": "multi-token decode, all experts resident: us per MoE layer, grouped GEMM vs per-token GEMV",
+        "metric": "multi-token decode, all experts resident: us per MoE layer, grouped GEMM vs per-token GEMV vs "
+                  "multi-token GEMV",
         "value": None, "unit": "us per layer", "n_gpus": 1, "higher_is_better": False, "data": "synthetic",
         "config": {"workload": wl.desc, "layers_timed": L, "tokens": "i.i.d. N(0,1)"},
         "rows": rows,

@@ -52,6 +52,8 @@ extern "C" {
 #define MOE_MAX_EXPERTS 256   /* n (experts per layer) upper bound */
 #define MOE_MAX_TOPK     16   /* k upper bound */
 #define MOE_MAX_D      8192   /* d_model upper bound of the GEMV kernels */
+#define MOE_MAX_TOKENS    8   /* tokens per call of moe_expert_ffn_tokens */
+#define MOE_TOKENS_LDS_BYTES 131072   /* moe_expert_ffn_tokens: T * d * 4 bytes at most */
 
 /* Message of the last failing call on the calling thread ("" if none). */
 const char *moe_last_error(void);
@@ -181,6 +183,27 @@ size_t moe_ffn_workspace_bytes(int max_jobs, int d, int f_max);
 int moe_expert_ffn_hits(const float *x, const void *slot_pool, int n_slots, const int32_t *hit_slots,
                         const float *hit_w, int n_hits, int d, int f, float *y,
                         void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Several decode tokens at once (a small batch), every selected expert resident:
+ *   y[t] = sum_j w[t][j] * FFN(slab at slot_pool + slots[t][j]*moe_slab_bytes(d,f), x[t])
+ * for t < T. Each slab is read from HBM once for all the tokens that selected it (the
+ * one-token path run per token would read it once per token). Not in the paper: the
+ * bridge between single-token decode and prefill.
+ * x          device fp32 [T][d]
+ * slot_pool  device bf16 slabs, n_slots of them
+ * slots      device int32 [T][k]; entries outside [0, n_slots) are skipped, and a slot
+ *            listed twice for one token is the caller's error (experts are distinct)
+ * w          device fp32 [T][k] gate weights
+ * y          device fp32 [T][d] (overwritten; zero for a token with no valid slot)
+ * workspace  device, 256-byte aligned, >= moe_ffn_tokens_workspace_bytes(T, k, d, f)
+ * 1 <= T <= MOE_MAX_TOKENS, 1 <= k <= MOE_MAX_TOPK, d % 8 == 0, d <= MOE_MAX_D,
+ * f % 8 == 0, T*d*4 <= MOE_TOKENS_LDS_BYTES; MOE_EINVAL otherwise.
+ */
+size_t moe_ffn_tokens_workspace_bytes(int T, int k, int d, int f);
+int moe_expert_ffn_tokens(const float *x, const void *slot_pool, int n_slots, const int32_t *slots,
+                          const float *w, int T, int k, int d, int f, float *y,
+                          void *workspace, size_t workspace_bytes, void *stream);
 
 /* ------------------------------------------------------------------------- */
 /* Weighted combine (Section I layer output; Section III-A hit/miss split).   */

@@ -16,12 +16,14 @@ import numpy as np
 
 from . import _abi
 from ._abi import LayerDesc, PrefillDesc, RuntimeStats
+from ._abi import MAX_D, MAX_EXPERTS, MAX_TOKENS, MAX_TOPK  # noqa: F401  (ABI bounds)
 
 _lib = _abi.load()
 
 __all__ = [
     "MoeError", "lib", "slab_bytes", "router_topk", "Cache", "ffn_workspace_bytes", "expert_ffn_hits",
     "combine", "PinnedBuffer", "HostPool", "Runtime", "prefill_workspace_bytes", "prefill_forward", "read_stream",
+    "ffn_tokens_workspace_bytes", "expert_ffn_tokens",
 ]
 
 
@@ -170,6 +172,20 @@ def expert_ffn_hits(x, slot_pool, n_slots, hit_slots, hit_w, d, f, y, workspace,
     n_hits = int(hit_slots.numel())
     _check("moe_expert_ffn_hits", _lib.moe_expert_ffn_hits(
         _ptr(x), _ptr(slot_pool), n_slots, _ptr(hit_slots), _ptr(hit_w), n_hits, d, f, _ptr(y),
+        _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
+    return y
+
+
+def ffn_tokens_workspace_bytes(T, k, d, f) -> int:
+    return int(_lib.moe_ffn_tokens_workspace_bytes(T, k, d, f))
+
+
+def expert_ffn_tokens(x, slot_pool, n_slots, slots, w, d, f, y, workspace, stream=None):
+    """y[t] = sum_j w[t][j] FFN(slot slots[t][j]) (x[t]) for T small-batch tokens, each
+    selected slab read once; x, y cuda fp32 [T, d], slots int32 / w fp32 cuda [T, k]."""
+    T, k = int(slots.shape[0]), int(slots.shape[1])
+    _check("moe_expert_ffn_tokens", _lib.moe_expert_ffn_tokens(
+        _ptr(x), _ptr(slot_pool), n_slots, _ptr(slots), _ptr(w), T, k, d, f, _ptr(y),
         _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
     return y
 

@@ -15,7 +15,7 @@ c_f32p = ctypes.POINTER(ctypes.c_float)
 c_char_p = ctypes.c_char_p
 
 MOE_OK, MOE_EINVAL, MOE_EHIP, MOE_ESTATE, MOE_ENOMEM = 0, -1, -2, -3, -4
-MAX_EXPERTS, MAX_TOPK, MAX_D = 256, 16, 8192
+MAX_EXPERTS, MAX_TOPK, MAX_D, MAX_TOKENS = 256, 16, 8192, 8
 
 
 class LayerDesc(ctypes.Structure):
@@ -66,6 +66,9 @@ SIGNATURES = [
     ("moe_expert_ffn_hits", c_int, [c_void_p, c_void_p, c_int, c_void_p, c_void_p, c_int, c_int, c_int,
                                     c_void_p, c_void_p, c_size_t, c_void_p]),
     ("moe_combine", c_int, [c_void_p, c_void_p, c_void_p, c_int, c_void_p, c_void_p]),
+    ("moe_ffn_tokens_workspace_bytes", c_size_t, [c_int, c_int, c_int, c_int]),
+    ("moe_expert_ffn_tokens", c_int, [c_void_p, c_void_p, c_int, c_void_p, c_void_p, c_int, c_int, c_int, c_int,
+                                      c_void_p, c_void_p, c_size_t, c_void_p]),
     ("moe_host_alloc", c_int, [c_size_t, ctypes.POINTER(c_void_p)]),
     ("moe_host_free", c_int, [c_void_p]),
     ("moe_host_pool_create", c_int, [c_int, ctypes.POINTER(c_void_p)]),

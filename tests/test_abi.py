@@ -55,6 +55,20 @@ def test_argument_errors_do_not_touch_the_device():
     assert lib.moe_expert_ffn_hits(None, None, 4, None, None, 17, 64, 64, None, None, 0, None) == _abi.MOE_EINVAL
     assert lib.moe_combine(None, None, None, 16, None, None) == _abi.MOE_EINVAL
     assert lib.moe_runtime_create(None, None) == _abi.MOE_EINVAL
+    # multi-token FFN: T, k, the staging limit and pointers checked before any HIP call
+    assert lib.moe_expert_ffn_tokens(None, None, 4, None, None, 0, 2, 256, 512, None, None, 0, None) == \
+        _abi.MOE_EINVAL
+    assert lib.moe_expert_ffn_tokens(None, None, 4, None, None, 9, 2, 256, 512, None, None, 0, None) == \
+        _abi.MOE_EINVAL
+    assert lib.moe_expert_ffn_tokens(None, None, 4, None, None, 8, 2, 8192, 512, None, None, 0, None) == \
+        _abi.MOE_EINVAL                                                    # 8 x 8192 floats > 128 KiB
+    assert b"staging" in lib.moe_last_error()
+    assert lib.moe_expert_ffn_tokens(None, None, 4, None, None, 2, 17, 256, 512, None, None, 0, None) == \
+        _abi.MOE_EINVAL
+    assert lib.moe_expert_ffn_tokens(None, None, 4, None, None, 2, 2, 256, 512, None, None, 0, None) == \
+        _abi.MOE_EINVAL                                                    # null pointers
+    assert lib.moe_ffn_tokens_workspace_bytes(0, 2, 256, 512) == 0
+    assert lib.moe_ffn_tokens_workspace_bytes(2, 2, 256, 512) >= 4 * 512 * 4 + 4 * 256 * 4
     # read-stream yardstick: size, grid and pointers checked before any HIP call
     assert lib.moe_read_stream(None, 24, None, 0, None) == _abi.MOE_EINVAL
     assert b"multiple of 16" in lib.moe_last_error()
