@@ -403,8 +403,9 @@ def measured_traffic(args):
     import hashlib
     try:
         rec = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))
-        src = open(os.path.join(ROOT, rec["kernel_source"]), "rb").read()
-    except (OSError, ValueError, KeyError):
+        # the kernel sources the counters were taken on, hashed in the listed order
+        src = b"".join(open(os.path.join(ROOT, f), "rb").read() for f in rec["kernel_sources"])
+    except (OSError, ValueError, KeyError, TypeError):
         return None
     want = {"workload": args.workload, "steps": args.steps, "warmup": args.warmup, "seed": args.seed}
     if hashlib.sha256(src).hexdigest() != rec.get("kernel_sha256") or rec.get("command_args") != want:
