@@ -439,6 +439,21 @@ def read_stream_yardstick(torch, moe, buf, launch_bytes):
     return out
 
 
+def measured_prefill_traffic(args):
+    """HBM bytes per prefill layer (the two grouped GEMMs) from the committed PMC record,
+    if it was taken on the current kernel source with the same workload and seed."""
+    import hashlib
+    try:
+        rec = json.load(open(os.path.join(ROOT, "profiles", "traffic_prefill.json")))
+        src = b"".join(open(os.path.join(ROOT, f), "rb").read() for f in rec["kernel_sources"])
+    except (OSError, ValueError, KeyError, TypeError):
+        return None
+    if (hashlib.sha256(src).hexdigest() != rec.get("kernel_sha256") or rec.get("workload") != args.workload
+            or rec.get("seed") != args.seed):
+        return None
+    return rec["hbm_bytes_per_layer"]
+
+
 def bench_prefill(args, torch, moe, synth, wl):
     """One prompt of wl.T tokens through every layer, all experts resident in HBM
     (L x n slabs, layers visited in order so no slab is reused while cached)."""
@@ -494,7 +509,9 @@ def bench_prefill(args, torch, moe, synth, wl):
                    "parallelism": "single GPU"},
         "roofline": {"kernel": "prefill layer (router, grouping, grouped MFMA GEMMs, combine)", "bound": "hbm",
                      "achieved": round(hbm, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(hbm / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(hbm / HBM_PEAK_GBS, 4), "traffic": measured_prefill_traffic(args),
+                     "traffic_unit": "HBM bytes per layer of the grouped GEMMs (rocprofv3 FETCH_SIZE x2.0 + "
+                                     "WRITE_SIZE, profiles/traffic_prefill.json)",
                      "mfma_tflops": round(tf, 1), "mfma_peak_tflops": 2500.0, "mfma_frac": round(tf / 2500.0, 4),
                      "us_per_layer": round(per_layer_us, 2)},
         "cpu_baseline": None,
