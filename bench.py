@@ -380,7 +380,12 @@ def small_batch_study(args, torch, moe, synth, wl):
         g_us = time_it(grouped) / L
         v_us = time_it(gemv, reps=2 if T >= 16 else 5) / L
         t_us = time_it(tokens) / L if T <= tmax_tok else None
-        touched = int(np.unique(idx[:T].cpu().numpy()).size)
+        # distinct experts per layer, averaged over the L timed layers (each reads its own)
+        per_layer = []
+        for l in range(L):
+            moe.router_topk(X[:T], wr[l], k, idx_out=idx[:T], w_out=wts[:T])
+            per_layer.append(int(np.unique(idx[:T].cpu().numpy()).size))
+        touched = sum(per_layer) / L
         rows.append({"T": T, "grouped_us_per_layer": round(g_us, 1), "gemv_us_per_layer": round(v_us, 1),
                      "tokens_us_per_layer": None if t_us is None else round(t_us, 1),
                      "experts_touched": touched,

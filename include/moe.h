@@ -189,7 +189,10 @@ int moe_expert_ffn_hits(const float *x, const void *slot_pool, int n_slots, cons
  *   y[t] = sum_j w[t][j] * FFN(slab at slot_pool + slots[t][j]*moe_slab_bytes(d,f), x[t])
  * for t < T. Each slab is read from HBM once for all the tokens that selected it (the
  * one-token path run per token would read it once per token). Not in the paper: the
- * bridge between single-token decode and prefill.
+ * bridge between single-token decode and prefill. The fp32 activations meet the bf16
+ * weights as two bf16 parts (hi + lo, within 2^-18 relative of the fp32 value) with
+ * exact products and fp32 sums, so results agree with the one-token path to fp32
+ * accumulation order.
  * x          device fp32 [T][d]
  * slot_pool  device bf16 slabs, n_slots of them
  * slots      device int32 [T][k]; entries outside [0, n_slots) are skipped, and a slot

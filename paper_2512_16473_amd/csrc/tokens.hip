@@ -12,6 +12,12 @@
 // weighted partials) -> reduce (fixed order). Every block builds the same job table
 // (distinct slots in order of first appearance; each job's (token, rank) pairs in order)
 // from the T*k selections.
+//
+// Each wave dots one weight row with several tokens, so the arithmetic per byte grows
+// with the tokens per slab. The hidden states are staged as two bf16 parts, hi = bf16(v)
+// and lo = bf16(v - hi) (|v - hi - lo| <= 2^-18 |v|), so that a 16-byte chunk of bf16
+// weights meets them through v_dot2_f32_bf16 (exact bf16 products, fp32 sums) without
+// widening the weights to fp32 once per token.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -30,6 +36,73 @@ constexpr int kMaxPairs = MOE_MAX_TOKENS * MOE_MAX_TOPK_INTERNAL;   // 128
 constexpr int kDownRows = 128;                           // W2 rows per down work group
 
 static_assert(kMaxPairs <= kTokThreads, "one thread per (token, rank) pair");
+static_assert(kMaxPairs <= 2 * kWave, "a wave keeps a job's pair results in two registers");
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// c + a[0] b[0] + a[1] b[1] over two packed bf16 pairs (element 0 in the low half)
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c)
+{
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), c, false);
+}
+
+// acc + dot(8 bf16 weights, 8 bf16 activation parts)
+__device__ __forceinline__ float dot8_bf(const uint4 w, const uint4 v, float acc)
+{
+    acc = dot2(w.x, v.x, acc);
+    acc = dot2(w.y, v.y, acc);
+    acc = dot2(w.z, v.z, acc);
+    return dot2(w.w, v.w, acc);
+}
+
+// Sum over the 64 lanes of a wave, returned to every lane. Cross-lane moves use DPP
+// (quad permutes, row mirrors, then row broadcasts of lanes 15 and 31, leaving the total
+// in lane 63): VALU operations, where a shuffle butterfly would make six dependent
+// round trips through the LDS crossbar per sum. Fixed order, so deterministic.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ float add_dpp(float v)
+{
+    // lanes of rows outside kRowMask add the `old` operand, 0
+    const int t = __builtin_amdgcn_update_dpp(0, __float_as_int(v), kCtrl, kRowMask, 0xF, false);
+    return v + __int_as_float(t);
+}
+
+__device__ __forceinline__ float wave_total(float v)
+{
+    v = add_dpp<0xB1, 0xF>(v);    // quad_perm [1,0,3,2]: pairs
+    v = add_dpp<0x4E, 0xF>(v);    // quad_perm [2,3,0,1]: quads
+    v = add_dpp<0x141, 0xF>(v);   // row_half_mirror: 8 lanes
+    v = add_dpp<0x140, 0xF>(v);   // row_mirror: the 16 lanes of a row
+    v = add_dpp<0x142, 0xA>(v);   // row_bcast:15 into rows 1 and 3: rows 0+1, 2+3
+    v = add_dpp<0x143, 0xC>(v);   // row_bcast:31 into rows 2 and 3: lane 63 holds the total
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+__device__ __forceinline__ uint32_t bf_bits(__bf16 v) { return __builtin_bit_cast(uint16_t, v); }
+
+// (a, b) -> packed hi parts and packed lo parts, both rounded to nearest even
+__device__ __forceinline__ void split2(float a, float b, uint32_t &hi, uint32_t &lo)
+{
+    const __bf16 ah = static_cast<__bf16>(a), bh = static_cast<__bf16>(b);
+    const __bf16 al = static_cast<__bf16>(a - static_cast<float>(ah));
+    const __bf16 bl = static_cast<__bf16>(b - static_cast<float>(bh));
+    hi = bf_bits(ah) | (bf_bits(bh) << 16);
+    lo = bf_bits(al) | (bf_bits(bl) << 16);
+}
+
+// 8 consecutive fp32 values -> one chunk of hi parts and one of lo parts
+__device__ __forceinline__ void split8(const float *src, uint4 *hi, uint4 *lo)
+{
+    const float4 v0 = reinterpret_cast<const float4 *>(src)[0];
+    const float4 v1 = reinterpret_cast<const float4 *>(src)[1];
+    uint4 h, l;
+    split2(v0.x, v0.y, h.x, l.x);
+    split2(v0.z, v0.w, h.y, l.y);
+    split2(v1.x, v1.y, h.z, l.z);
+    split2(v1.z, v1.w, h.w, l.w);
+    *hi = h;
+    *lo = l;
+}
 
 struct TokJobs {
     int njobs;
@@ -105,12 +178,18 @@ struct TokParams {
 template <int CPL>
 __global__ __launch_bounds__(kTokThreads) void k_tok_gate_up(TokParams p)
 {
+    constexpr int kPitch = CPL * kWave;   // chunks per token row in LDS
     __shared__ TokJobs J;
-    extern __shared__ float4 xs4[];   // [T][d] fp32, 16-byte aligned
-    float *xs = reinterpret_cast<float *>(xs4);
+    extern __shared__ uint4 xs4[];        // hi parts [T][kPitch], then lo parts [T][kPitch]
     build_jobs(p.slots, p.T * p.k, p.nslots, J);
-    const int d = p.d, nch = d >> 3;
-    for (int i = threadIdx.x; i < p.T * d / 4; i += kTokThreads) xs4[i] = reinterpret_cast<const float4 *>(p.x)[i];
+    const int d = p.d, nch = d >> 3, lo_off = p.T * kPitch;
+    // chunks past d/8 hold zeros: a lane's last chunk, whose weights are re-read from the
+    // row's last chunk, then adds nothing, and every chunk is dotted without a branch
+    for (int i = threadIdx.x; i < lo_off; i += kTokThreads) {
+        const int t = i / kPitch, e = i - t * kPitch;
+        if (e < nch) split8(p.x + (size_t)t * d + e * 8, xs4 + i, xs4 + lo_off + i);
+        else xs4[i] = xs4[lo_off + i] = make_uint4(0, 0, 0, 0);
+    }
     __syncthreads();
 
     const int lane = threadIdx.x & (kWave - 1);
@@ -118,7 +197,12 @@ __global__ __launch_bounds__(kTokThreads) void k_tok_gate_up(TokParams p)
     const int total = J.njobs * p.f;
     // Two register sets: the next row pair is in flight while this one is dotted with
     // the tokens. Loads are unconditional (past the end they re-read the last row pair)
-    // so that each wait covers only the older set.
+    // so that each wait covers only the older set. Every path through the dot reads every
+    // register of its set (a do-while over the pairs, no per-chunk branch): a register left
+    // unread on some path, or a loop that stores to global memory while reading registers
+    // still being loaded, makes the compiler wait for every outstanding load, the
+    // prefetched set included. Lane j keeps the result of the job's pair j (j + 64 in h1_)
+    // and the stores follow the pair loop.
     uint4 a[2][CPL], b[2][CPL];
 #define MOE_TOK_LOAD(set, item)                                                                        \
     do {                                                                                               \
@@ -135,32 +219,45 @@ __global__ __launch_bounds__(kTokThreads) void k_tok_gate_up(TokParams p)
     } while (0)
 #define MOE_TOK_DOT(set, item)                                                                         \
     do {                                                                                               \
-        const int job_ = (item) / p.f, i_ = (item) - job_ * p.f;                                        \
-        for (int q = J.first[job_]; q < J.first[job_ + 1]; ++q) {                                      \
-            const int pr = J.pair[q];                                                                  \
-            const float *xt = xs + (pr / p.k) * d;                                                     \
-            float g = 0.f, u = 0.f;                                                                    \
+        const bool live_ = (item) < total;                                                             \
+        const int it_ = min((item), total - 1);                                                        \
+        const int job_ = it_ / p.f, i_ = it_ - job_ * p.f;                                              \
+        const int q0_ = J.first[job_], nq_ = live_ ? J.first[job_ + 1] - q0_ : 1;                      \
+        float h0_ = 0.f, h1_ = 0.f;                                                                    \
+        int q = 0;                                                                                     \
+        do {                                                                                           \
+            const uint4 *xt = xs4 + (J.pair[q0_ + q] / p.k) * kPitch + lane;                           \
+            float gh = 0.f, gl = 0.f, uh = 0.f, ul = 0.f;                                              \
             _Pragma("unroll") for (int c = 0; c < CPL; ++c) {                                          \
-                const int ch = c * kWave + lane;                                                       \
-                if (ch < nch) {                                                                        \
-                    float xv[8];                                                                       \
-                    load8(xt + ch * 8, xv);                                                            \
-                    g = dot8(a[set][c], xv, g);                                                        \
-                    u = dot8(b[set][c], xv, u);                                                        \
-                }                                                                                      \
+                const uint4 xh = xt[c * kWave], xl = xt[lo_off + c * kWave];                           \
+                gh = dot8_bf(a[set][c], xh, gh);                                                       \
+                gl = dot8_bf(a[set][c], xl, gl);                                                       \
+                uh = dot8_bf(b[set][c], xh, uh);                                                       \
+                ul = dot8_bf(b[set][c], xl, ul);                                                       \
             }                                                                                          \
-            g = wave_sum(g);                                                                           \
-            u = wave_sum(u);                                                                           \
-            if (lane == 0) p.h[(size_t)pr * p.f + i_] = g / (1.0f + expf(-g)) * u;                      \
-        }                                                                                              \
+            const float g = wave_total(gh + gl);                                                         \
+            const float u = wave_total(uh + ul);                                                         \
+            const float hv = g / (1.0f + expf(-g)) * u;                                                \
+            if (lane == (q & (kWave - 1))) {                                                           \
+                if (q < kWave) h0_ = hv;                                                               \
+                else h1_ = hv;                                                                         \
+            }                                                                                          \
+        } while (++q < nq_);   /* a job has at least one pair */                                       \
+        const int ns_ = live_ ? nq_ : 0;                                                               \
+        if (lane < ns_) p.h[(size_t)J.pair[q0_ + lane] * p.f + i_] = h0_;                              \
+        if (lane + kWave < ns_) p.h[(size_t)J.pair[q0_ + kWave + lane] * p.f + i_] = h1_;              \
     } while (0)
 
-    int it = blockIdx.x * kTokWaves + (threadIdx.x >> 6);
+    // The loop control is uniform (the wave index through readfirstlane) and has no exit
+    // between the halves: an item past the end in the second half is dotted (one pair,
+    // the loaded last row) but not stored. A mid-loop exit, or a divergent one, is a path
+    // to the loop head that skips the second dot, and the compiler would again wait for
+    // both sets there.
+    int it = blockIdx.x * kTokWaves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     if (it < total) MOE_TOK_LOAD(0, it);
     for (; it < total; it += 2 * nwaves) {
         MOE_TOK_LOAD(1, it + nwaves);
         MOE_TOK_DOT(0, it);
-        if (it + nwaves >= total) break;
         MOE_TOK_LOAD(0, it + 2 * nwaves);
         MOE_TOK_DOT(1, it + nwaves);
     }
@@ -175,9 +272,9 @@ __global__ __launch_bounds__(kTokThreads) void k_tok_gate_up(TokParams p)
 template <int CPK>
 __global__ __launch_bounds__(kTokThreads) void k_tok_down(TokParams p)
 {
+    constexpr int kPitch = CPK * kWave;   // chunks per staged pair row in LDS
     __shared__ TokJobs J;
-    extern __shared__ float4 hs4[];   // [pairs of the job][seg] fp32, 16-byte aligned
-    float *hs = reinterpret_cast<float *>(hs4);
+    extern __shared__ uint4 hs4[];        // hi parts [T][kPitch], then lo parts [T][kPitch]
     build_jobs(p.slots, p.T * p.k, p.nslots, J);
     const int nchunk = (p.d + kDownRows - 1) / kDownRows;
     const int job = blockIdx.x / (p.nseg * nchunk);
@@ -188,6 +285,7 @@ __global__ __launch_bounds__(kTokThreads) void k_tok_down(TokParams p)
     const int len = min(p.seg, p.f - c0);
     const int nch = len >> 3;
     const int q0 = J.first[job], np = J.first[job + 1] - q0;
+    const int lo_off = p.T * kPitch;
     const int lane = threadIdx.x & (kWave - 1);
     const uint8_t *w2 = p.pool + (uint64_t)J.slot[job] * p.slab_stride + (uint64_t)2 * p.f * p.d * 2;
     const int r1 = min(r0 + kDownRows, p.d);
@@ -196,11 +294,17 @@ __global__ __launch_bounds__(kTokThreads) void k_tok_down(TokParams p)
     for (int qc = 0; qc < np; qc += p.T) {
         const int nq = min(p.T, np - qc);
         if (qc) __syncthreads();   // the previous group's segments are no longer read
-        for (int i = threadIdx.x; i < nq * (len / 4); i += kTokThreads) {
-            const int q = i / (len / 4), e = i - q * (len / 4);
-            hs4[(q * p.seg) / 4 + e] = reinterpret_cast<const float4 *>(p.h + (size_t)J.pair[q0 + qc + q] * p.f + c0)[e];
+        // chunks past the segment's end hold zeros (see k_tok_gate_up)
+        for (int i = threadIdx.x; i < nq * kPitch; i += kTokThreads) {
+            const int q = i / kPitch, e = i - q * kPitch;
+            if (e < nch) split8(p.h + (size_t)J.pair[q0 + qc + q] * p.f + c0 + e * 8, hs4 + i, hs4 + lo_off + i);
+            else hs4[i] = hs4[lo_off + i] = make_uint4(0, 0, 0, 0);
         }
         __syncthreads();
+        // lane q < nq holds pair q's id and combine weight, and keeps its dot product;
+        // the stores follow the pair loop (see k_tok_gate_up)
+        const int pr_l = lane < nq ? J.pair[q0 + qc + lane] : 0;
+        const float w_l = lane < nq ? p.w[pr_l] : 0.f;
         // rows r, r + 8, ... of this group, two register sets (the next row's segment in
         // flight while this one is dotted); loads past the last row re-read it
         uint4 a[2][CPK];
@@ -211,30 +315,29 @@ __global__ __launch_bounds__(kTokThreads) void k_tok_down(TokParams p)
         } while (0)
 #define MOE_TOK_DOT_ROW(set, rr)                                                                       \
         do {                                                                                           \
-            for (int q = 0; q < nq; ++q) {                                                             \
-                const float *ht = hs + q * p.seg;                                                      \
-                float acc = 0.f;                                                                       \
+            const bool live_ = (rr) < r1;                                                              \
+            const int nl_ = live_ ? nq : 1;                                                            \
+            float o_ = 0.f;                                                                            \
+            int q = 0;                                                                                 \
+            do {                                                                                       \
+                const uint4 *ht = hs4 + q * kPitch + lane;                                             \
+                float ah = 0.f, al = 0.f;                                                              \
                 _Pragma("unroll") for (int c = 0; c < CPK; ++c) {                                      \
-                    const int ch = c * kWave + lane;                                                   \
-                    if (ch < nch) {                                                                    \
-                        float hv[8];                                                                   \
-                        load8(ht + ch * 8, hv);                                                        \
-                        acc = dot8(a[set][c], hv, acc);                                                \
-                    }                                                                                  \
+                    ah = dot8_bf(a[set][c], ht[c * kWave], ah);                                        \
+                    al = dot8_bf(a[set][c], ht[lo_off + c * kWave], al);                               \
                 }                                                                                      \
-                acc = wave_sum(acc);                                                                   \
-                if (lane == 0) {                                                                       \
-                    const int pr = J.pair[q0 + qc + q];                                                \
-                    p.partial[((size_t)pr * p.nseg + sgi) * p.d + (rr)] = p.w[pr] * acc;               \
-                }                                                                                      \
-            }                                                                                          \
+                const float acc = wave_total(ah + al);                                                   \
+                if (lane == q) o_ = acc;                                                               \
+            } while (++q < nl_);                                                                       \
+            if (live_ && lane < nq) p.partial[((size_t)pr_l * p.nseg + sgi) * p.d + (rr)] = w_l * o_;  \
         } while (0)
-        int r = r0 + (threadIdx.x >> 6);
+        // uniform loop control without a mid-loop exit; a row past the end is dotted with
+        // one pair and not stored (see k_tok_gate_up)
+        int r = r0 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
         if (r < r1) MOE_TOK_LOAD_ROW(0, r);
         for (; r < r1; r += 2 * kTokWaves) {
             MOE_TOK_LOAD_ROW(1, r + kTokWaves);
             MOE_TOK_DOT_ROW(0, r);
-            if (r + kTokWaves >= r1) break;
             MOE_TOK_LOAD_ROW(0, r + 2 * kTokWaves);
             MOE_TOK_DOT_ROW(1, r + kTokWaves);
         }
@@ -319,7 +422,8 @@ hipError_t launch_tokens(const float *x, const uint8_t *pool, uint64_t stride, i
     hipError_t e;
     // gate/up: grid-stride over (job, row), one round of resident work groups
     const int cpl = (d / 8 + kWave - 1) / kWave;
-    const size_t lds_x = (size_t)T * d * sizeof(float);
+    // T rows of cpl * 64 chunks, each chunk 16 bytes of hi parts and 16 of lo parts
+    const size_t lds_x = (size_t)T * cpl * kWave * 32;
     const int gu_grid = 0;
     switch (cpl) {
 #define MOE_TOK_CPL(N) \
@@ -334,8 +438,8 @@ hipError_t launch_tokens(const float *x, const uint8_t *pool, uint64_t stride, i
     // down: one work group per (job, segment, kDownRows rows); groups past the job count exit
     const int nchunk = (d + kDownRows - 1) / kDownRows;
     const int dn_grid = max_jobs * p.nseg * nchunk;
-    const size_t lds_h = (size_t)T * p.seg * sizeof(float);
     const int cpk = (p.seg / 8 + kWave - 1) / kWave;
+    const size_t lds_h = (size_t)T * cpk * kWave * 32;
     if (dn_grid > 0) {
         switch (cpk) {
 #define MOE_TOK_CPK(N) \
