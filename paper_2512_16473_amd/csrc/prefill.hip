@@ -39,6 +39,8 @@ constexpr int kRowChunks = kBK / 8;  // 16-byte chunks of a token row per step
 constexpr int kXcds = 8;
 constexpr int kSpreadTokens = 64;   // below this many (token, expert) pairs per expert, spread items over XCDs
 constexpr int kMaxDownSplits = 4;
+constexpr int kMaxTailSlots = 32;   // gate/up tail: work groups per XCD the split tiles may use
+constexpr int kMaxTailSplit = 16;   // gate/up tail: K parts per split tile
 
 __device__ __forceinline__ uint16_t f2bf(float f)
 {
@@ -129,6 +131,9 @@ struct GemmArgs {
     int ksplit;               // K splits
     int per_xcd;              // work items per XCD (expert-per-XCD layout)
     int spread;               // 1: item b is simply the b-th (expert, m, n, k) item
+    int tail;                 // gate/up, expert-per-XCD layout: split the last partial round over K
+    int slots;                // tail: work groups resident per XCD (<= kMaxTailSlots)
+    float *part;              // tail: fp32 (g, u) partial sums [8][slots][kTileM][2 * 16 kWaves]
     uint16_t *h;              // gate/up output, bf16 [P][f]
     float *yp;                // down output, fp32 [ksplit][P][d]
 };
@@ -188,13 +193,18 @@ __device__ __forceinline__ void gemm_k_loop(uint16_t (*lds_a)[kTileM * kLdsStrid
 {
     static_assert(!kRowLoads || kBK == 64, "row-contiguous weight loads cover 128 bytes of a row per step");
     constexpr int kLB = kRowLoads ? 2 * kNB : kNB * kKBlocks;   // weight loads per lane per step
+    // only the NMB token blocks that hold tokens are staged (the first kAL of the thread's
+    // kAN chunks): a tile of 128 tokens stages 128 rows per step, not 192
+    constexpr int kChunks = NMB * 16 * kRowChunks;
+    constexpr int kAL = (kChunks + kThr - 1) / kThr;
+    static_assert(kAL <= kAN, "staged chunks within the tile's");
     const int tid = threadIdx.x, lane = tid & 63;
-    u32x4_t ra[kS][kAN], rb[kS][kLB];
+    u32x4_t ra[kS][kAL], rb[kS][kLB];
     u32x4_t rt[kRowLoads ? kNB * kKBlocks : 1];                 // operand pieces after the LDS pass
 #define MOE_LOAD(set, step)                                                                           \
     do {                                                                                              \
         const int ko_ = min((step), nsteps - 1) * kBK;                                                \
-        _Pragma("unroll") for (int i = 0; i < kAN; ++i) ra[set][i] =                                \
+        _Pragma("unroll") for (int i = 0; i < kAL; ++i) ra[set][i] =                                \
             *reinterpret_cast<const u32x4_t *>(asrc[i] + ko_);                                        \
         if constexpr (kRowLoads) {                                                                    \
             _Pragma("unroll") for (int i = 0; i < kLB; ++i) rb[set][i] =                              \
@@ -207,9 +217,9 @@ __device__ __forceinline__ void gemm_k_loop(uint16_t (*lds_a)[kTileM * kLdsStrid
     } while (0)
 #define MOE_STASH(set, buf)                                                                           \
     do {                                                                                              \
-        _Pragma("unroll") for (int i = 0; i < kAN; ++i) {                                           \
+        _Pragma("unroll") for (int i = 0; i < kAL; ++i) {                                           \
             const int c_ = tid + kThr * i;                                                       \
-            if (kTileM * kRowChunks % kThr == 0 || c_ < kTileM * kRowChunks)                          \
+            if (kChunks % kThr == 0 || c_ < kChunks)                                                  \
                 *reinterpret_cast<u32x4_t *>(&lds_a[buf][(c_ / kRowChunks) * kLdsStride + (c_ % kRowChunks) * 8]) = ra[set][i]; \
         }                                                                                             \
     } while (0)
@@ -260,6 +270,40 @@ __device__ __forceinline__ void gemm_k_loop(uint16_t (*lds_a)[kTileM * kLdsStrid
 #undef MOE_MMA
 }
 
+// Gate/up tail split (expert-per-XCD layout). The live tiles of XCD x (its experts x,
+// x + 8, ... times their occupied M tiles and the N tiles) run in rounds of g.slots work
+// groups; the r tiles of a last, partial round are split over K into s parts, as many as
+// the idle work groups allow (s r <= slots), and a second kernel adds the parts.
+struct TailPlan {
+    int U, R, r, s;   // live tiles, full rounds, tiles of the partial round, K parts per tile
+};
+
+__device__ __forceinline__ TailPlan tail_plan(const GemmArgs &g, int xcd)
+{
+    TailPlan p;
+    p.U = 0;
+    for (int e = xcd; e < g.n; e += kXcds) p.U += (g.off[e + 1] - g.off[e] + kTileM - 1) / kTileM * g.ntiles;
+    p.R = p.U / g.slots;
+    p.r = p.U - p.R * g.slots;
+    p.s = 1;
+    while (p.r > 0 && 2 * p.s * p.r <= g.slots && 2 * p.s <= kMaxTailSplit && (g.d / kBK) % (2 * p.s) == 0) p.s *= 2;
+    return p;
+}
+
+// live tile t (< U) of XCD xcd -> expert, M tile, N tile (N-major within an expert)
+__device__ __forceinline__ void tail_tile(const GemmArgs &g, int xcd, int t, int &e, int &mt, int &nt)
+{
+    for (e = xcd;; e += kXcds) {
+        const int m_e = (g.off[e + 1] - g.off[e] + kTileM - 1) / kTileM;
+        if (t < m_e * g.ntiles) {
+            mt = t % m_e;
+            nt = t / m_e;
+            return;
+        }
+        t -= m_e * g.ntiles;
+    }
+}
+
 template <bool kGateUp, int kS, int kNB, int kWaves>
 __global__ __launch_bounds__(kWaves * 64) void k_moe_gemm(GemmArgs g)
 {
@@ -269,28 +313,51 @@ __global__ __launch_bounds__(kWaves * 64) void k_moe_gemm(GemmArgs g)
     __shared__ uint16_t lds_a[2][kTileM * kLdsStride];
     __shared__ uint16_t lds_w[kRowLoads ? kWaves : 1][kRowLoads ? 16 * kNB * kWStride : 8];
 
-    const int per_expert = g.mtiles * g.ntiles * g.ksplit;
-    int q, e;
-    if (g.spread) {   // few tokens per expert: an expert's items go round all XCDs
-        q = blockIdx.x;
-        e = q / per_expert;
-    } else {          // an expert's items stay on XCD e mod 8, sharing its token rows in L2
-        q = blockIdx.x / kXcds;
-        if (q >= g.per_xcd) return;
-        e = blockIdx.x % kXcds + kXcds * (q / per_expert);
+    const int K = kGateUp ? g.d : g.f;
+    int e, mt, nt, ks = 0, kparts = g.ksplit;
+    int xcd = 0, tail_v = -1, tail_s = 1;   // tail: unit v of a tile split in tail_s K parts
+    if (kGateUp && g.tail) {
+        // units: the full tiles (whole K) first, then the K parts of the partial round's tiles
+        xcd = blockIdx.x % kXcds;
+        const int u = blockIdx.x / kXcds;
+        const TailPlan tp = tail_plan(g, xcd);
+        tail_s = tp.s;
+        int t;
+        if (u < tp.R * g.slots || tail_s == 1) {
+            if (u >= tp.U) return;
+            t = u;
+        } else {
+            const int v = u - tp.R * g.slots;
+            if (v >= tp.r * tail_s) return;
+            t = tp.R * g.slots + v / tail_s;
+            ks = v % tail_s;
+            kparts = tail_s;
+            tail_v = v;
+        }
+        tail_tile(g, xcd, t, e, mt, nt);
+    } else {
+        const int per_expert = g.mtiles * g.ntiles * g.ksplit;
+        int q;
+        if (g.spread) {   // few tokens per expert: an expert's items go round all XCDs
+            q = blockIdx.x;
+            e = q / per_expert;
+        } else {          // an expert's items stay on XCD e mod 8, sharing its token rows in L2
+            q = blockIdx.x / kXcds;
+            if (q >= g.per_xcd) return;
+            e = blockIdx.x % kXcds + kXcds * (q / per_expert);
+        }
+        if (e >= g.n) return;
+        q %= per_expert;
+        ks = q % g.ksplit;
+        q /= g.ksplit;
+        mt = q % g.mtiles;
+        nt = q / g.mtiles;
     }
-    if (e >= g.n) return;
-    q %= per_expert;
-    const int ks = q % g.ksplit;
-    q /= g.ksplit;
-    const int mt = q % g.mtiles;
-    const int nt = q / g.mtiles;
     const int row0 = g.off[e] + mt * kTileM;
     const int rows = min(kTileM, g.off[e + 1] - row0);
     if (rows <= 0) return;
 
-    const int K = kGateUp ? g.d : g.f;
-    const int kspan = K / g.ksplit;
+    const int kspan = K / kparts;
     const int k0 = ks * kspan;
     const int nsteps = kspan / kBK;
     const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
@@ -342,6 +409,22 @@ __global__ __launch_bounds__(kWaves * 64) void k_moe_gemm(GemmArgs g)
     }
 
     // Output element r of a 16x16 block sits at row 4*(lane/16) + r, column lane%16.
+    if constexpr (kGateUp) {
+        if (tail_v >= 0) {   // a K part of a split tile: its fp32 (g, u) sums, added by k_tail_combine
+            constexpr int kCols = 2 * kWaves * 16;   // g columns, then u columns
+            float *mine = g.part + ((size_t)xcd * g.slots + tail_v) * kTileM * kCols;
+#pragma unroll
+            for (int m = 0; m < kMBlocks; ++m)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int tr = m * 16 + 4 * (lane >> 4) + r;
+                    if (tr >= rows) continue;
+                    mine[tr * kCols + wv * 16 + (lane & 15)] = acc[m][0][r];
+                    mine[tr * kCols + kWaves * 16 + wv * 16 + (lane & 15)] = acc[m][kNB - 1][r];
+                }
+            return;
+        }
+    }
     const int P = g.off[g.n];
 #pragma unroll
     for (int m = 0; m < kMBlocks; ++m) {
@@ -360,6 +443,43 @@ __global__ __launch_bounds__(kWaves * 64) void k_moe_gemm(GemmArgs g)
                 for (int nb = 0; nb < kNB; ++nb) dst[16 * nb] = acc[m][nb][r];
             }
         }
+    }
+}
+
+// H of the gate/up tiles split over K: h = SiLU(sum of the g parts) * (sum of the u parts),
+// the parts added in order. Work group b: XCD b mod 8, then tile i of that XCD's partial
+// round and a block of 16 of its rows (the plan is recomputed from the expert offsets
+// exactly as the GEMM did); each thread takes 4 consecutive columns of 2 rows.
+constexpr int kTailRows = 16;
+__global__ __launch_bounds__(kThreads) void k_tail_combine(GemmArgs g)
+{
+    constexpr int kCols = 2 * kGWaves * 16;   // g columns, then u columns
+    constexpr int kQuads = kGWaves * 16 / 4;  // 4-column groups of the tile's 128 columns
+    const int xcd = blockIdx.x % kXcds;
+    const int i = (blockIdx.x / kXcds) % g.slots;
+    const int rb = blockIdx.x / kXcds / g.slots;
+    const TailPlan tp = tail_plan(g, xcd);
+    if (tp.s == 1 || i >= tp.r) return;
+    int e, mt, nt;
+    tail_tile(g, xcd, tp.R * g.slots + i, e, mt, nt);
+    const int row0 = g.off[e] + mt * kTileM;
+    const int rows = min(kTileM, g.off[e + 1] - row0);
+    const float *p0 = g.part + ((size_t)xcd * g.slots + (size_t)i * tp.s) * kTileM * kCols;
+    for (int c = threadIdx.x; c < kTailRows * kQuads; c += kThreads) {
+        const int tr = rb * kTailRows + c / kQuads, col = (c % kQuads) * 4;
+        if (tr >= rows) continue;
+        float4 gv = make_float4(0.f, 0.f, 0.f, 0.f), uv = gv;
+        for (int j = 0; j < tp.s; ++j) {
+            const float *pj = p0 + (size_t)j * kTileM * kCols + tr * kCols + col;
+            const float4 a = *reinterpret_cast<const float4 *>(pj);
+            const float4 b = *reinterpret_cast<const float4 *>(pj + kCols / 2);
+            gv.x += a.x; gv.y += a.y; gv.z += a.z; gv.w += a.w;
+            uv.x += b.x; uv.y += b.y; uv.z += b.z; uv.w += b.w;
+        }
+        uint2 o;
+        o.x = f2bf(gv.x / (1.0f + expf(-gv.x)) * uv.x) | ((uint32_t)f2bf(gv.y / (1.0f + expf(-gv.y)) * uv.y) << 16);
+        o.y = f2bf(gv.z / (1.0f + expf(-gv.z)) * uv.z) | ((uint32_t)f2bf(gv.w / (1.0f + expf(-gv.w)) * uv.w) << 16);
+        *reinterpret_cast<uint2 *>(g.h + (size_t)(row0 + tr) * g.f + nt * (kGWaves * 16) + col) = o;
     }
 }
 
@@ -402,7 +522,14 @@ struct PrefillWs {
     float *w;
     uint16_t *h;
     float *yp;
+    float *part;   // gate/up tail partial sums (expert-per-XCD layout only)
 };
+
+// Few (token, expert) pairs per expert: every expert's items are spread over all XCDs.
+bool spread_layout(int n, int k, int T) { return (int64_t)T * k < (int64_t)kSpreadTokens * n; }
+
+// fp32 (g, u) partial sums of the gate/up tiles split over K: [8][kMaxTailSlots][kTileM][2 * 128]
+constexpr size_t kPartBytes = (size_t)kXcds * kMaxTailSlots * kTileM * 2 * kGWaves * 16 * sizeof(float);
 
 size_t layout(int d, int f, int n, int k, int T, uint8_t *base, PrefillWs *ws)
 {
@@ -421,6 +548,7 @@ size_t layout(int d, int f, int n, int k, int T, uint8_t *base, PrefillWs *ws)
     uint8_t *pos = take(P * 4);
     uint8_t *h = take(P * f * 2);
     uint8_t *yp = take((size_t)kMaxDownSplits * P * d * 4);
+    uint8_t *part = take(spread_layout(n, k, T) ? 0 : kPartBytes);
     if (ws) {
         ws->xb = reinterpret_cast<uint16_t *>(xb);
         ws->idx = reinterpret_cast<int32_t *>(idx);
@@ -430,6 +558,7 @@ size_t layout(int d, int f, int n, int k, int T, uint8_t *base, PrefillWs *ws)
         ws->pos = reinterpret_cast<int32_t *>(pos);
         ws->h = reinterpret_cast<uint16_t *>(h);
         ws->yp = reinterpret_cast<float *>(yp);
+        ws->part = reinterpret_cast<float *>(part);
     }
     return o;
 }
@@ -471,7 +600,7 @@ hipError_t launch_prefill(const PrefillPlan &P, const float *X, float *OUT, int3
     const int groups = (P.n + kXcds - 1) / kXcds;
     // With few tokens per expert most experts are idle or nearly so, and keeping an
     // expert on one XCD would leave the others without work; spread its tiles instead.
-    g.spread = (int64_t)P.T * P.k < (int64_t)kSpreadTokens * P.n;
+    g.spread = spread_layout(P.n, P.k, P.T);
     auto grid_of = [&](const GemmArgs &a) {
         return g.spread ? P.n * a.mtiles * a.ntiles * a.ksplit : kXcds * a.per_xcd;
     };
@@ -481,10 +610,31 @@ hipError_t launch_prefill(const PrefillPlan &P, const float *X, float *OUT, int3
     g.ntiles = P.f / (kGWaves * 16);
     g.ksplit = 1;
     g.per_xcd = groups * g.mtiles * g.ntiles * g.ksplit;
-    hipLaunchKernelGGL((k_moe_gemm<true, 4, 2, kGWaves>), dim3(grid_of(g)), dim3(kGWaves * 64), 0, s, g);
+    // Tail splitting (expert-per-XCD layout): the rounds of resident work groups per XCD
+    // decide which tiles are split.
+    static int gu_occ = -1;
+    if (gu_occ < 0 && (hipOccupancyMaxActiveBlocksPerMultiprocessor(&gu_occ, k_moe_gemm<true, 4, 2, kGWaves>,
+                                                                     kGWaves * 64, 0) != hipSuccess || gu_occ < 1)) {
+        (void)hipGetLastError();
+        gu_occ = 0;
+    }
+    const int slots = std::min(kMaxTailSlots, gu_occ * device_cu_count() / kXcds);
+    g.tail = !g.spread && slots >= 2;
+    g.slots = g.tail ? slots : 0;
+    g.part = ws.part;
+    // with tail splitting a work group takes a live tile or a K part of one: at most the
+    // live tiles plus one round of parts
+    const int gu_per_xcd = g.tail ? g.per_xcd + g.slots : g.per_xcd;
+    const int gu_grid = g.spread ? grid_of(g) : kXcds * gu_per_xcd;
+    hipLaunchKernelGGL((k_moe_gemm<true, 4, 2, kGWaves>), dim3(gu_grid), dim3(kGWaves * 64), 0, s, g);
     if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (g.tail) {
+        hipLaunchKernelGGL(k_tail_combine, dim3(kXcds * g.slots * (kTileM / kTailRows)), dim3(kThreads), 0, s, g);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
 
     // down: 256 (or 128) output rows per work group, K = f split in 4 (or 2) parts
+    g.tail = 0;
     g.a = ws.h;
     g.ksplit = down_splits(P.f);
     const bool wide = P.d % (kGWaves * 32) == 0;

@@ -55,10 +55,14 @@ def _pool_np(torch, slabs, d, f):
 
 # (256, 512, 4, 2, 700): 1400 pairs (two chunks of the grouping sort) and ~350 tokens per
 # expert (two 192-token tiles); (384, 640, ...): d not a multiple of 256 (128-row down tiles)
-# and f not a multiple of 256 (two K splits).
+# and f not a multiple of 256 (two K splits). With one expert per XCD and 32 gate/up work
+# groups resident per XCD, the gate/up tiles of the last partial round are split over K:
+# (512, 1024, 8, 2, 300) 8 tiles per XCD in 4 parts each; (256, 512, 4, 2, 700) two M tiles
+# per expert, 4 parts; (256, 5120, 8, 2, 256) a full round of 32 tiles, then 8 tiles in 4
+# parts; (256, 1024, 16, 2, 520) two experts per XCD, 16 tiles in 2 parts.
 @pytest.mark.parametrize("d,f,n,k,T", [(256, 512, 4, 2, 64), (256, 512, 4, 2, 37), (512, 1024, 8, 2, 300),
                                        (384, 640, 16, 4, 130), (256, 256, 8, 1, 1), (256, 512, 64, 8, 48),
-                                       (256, 512, 4, 2, 700)])
+                                       (256, 512, 4, 2, 700), (256, 5120, 8, 2, 256), (256, 1024, 16, 2, 520)])
 def test_prefill_small(d, f, n, k, T):
     torch = torch_cuda()
     say("prefill", d, f, n, k, T)
