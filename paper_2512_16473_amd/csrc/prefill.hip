@@ -6,7 +6,9 @@
 //      giving per-expert offsets, the sorted pair list and its inverse;
 //   3. hidden states rounded to bf16 for the matrix cores;
 //   4. grouped GEMM gate/up: for each expert e, H_e = SiLU(X_e W1_e^T) * (X_e W3_e^T),
-//      bf16 MFMA (v_mfma_f32_16x16x32_bf16) with fp32 accumulation, H_e stored bf16;
+//      bf16 MFMA (v_mfma_f32_16x16x32_bf16) with fp32 accumulation, H_e stored bf16; the
+//      tiles of a last, partial round of work groups are split over K, and
+//   4b. a small kernel adds their parts and applies SiLU * up;
 //   5. grouped GEMM down: Y_e = H_e W2_e^T, K split in four (or two), fp32 partials;
 //   6. combine: OUT[t] = sum_r w[t][r] * Y[pair(t, r)], in a fixed order.
 //
