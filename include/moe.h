@@ -195,8 +195,9 @@ int moe_expert_ffn_hits(const float *x, const void *slot_pool, int n_slots, cons
  * accumulation order.
  * x          device fp32 [T][d]
  * slot_pool  device bf16 slabs, n_slots of them
- * slots      device int32 [T][k]; entries outside [0, n_slots) are skipped, and a slot
- *            listed twice for one token is the caller's error (experts are distinct)
+ * slots      device int32 [T][k]; entries outside [0, n_slots) are skipped; a slot listed
+ *            more than once (by one token or several) contributes once per listing, each
+ *            with its own weight (routing gives distinct experts per token)
  * w          device fp32 [T][k] gate weights
  * y          device fp32 [T][d] (overwritten; zero for a token with no valid slot)
  * workspace  device, 256-byte aligned, >= moe_ffn_tokens_workspace_bytes(T, k, d, f)

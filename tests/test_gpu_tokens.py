@@ -103,6 +103,30 @@ def test_tokens_invalid_slots_and_single_token():
     assert_close(y1[0], yh.cpu().numpy(), "T=1 vs hit path")
 
 
+@pytest.mark.parametrize("T,k,nslots,pattern", [
+    (2, 4, 3, "dup"),        # a job with 6 pairs for T = 2: h staged in three groups of T
+    (8, 16, 2, "one"),       # 128 pairs of one slot: results past the 64th pair, eight groups
+])
+def test_tokens_repeated_slots(T, k, nslots, pattern):
+    """A slot listed several times (also by one token) contributes once per listing, each
+    with its own weight: the job then has more (token, rank) pairs than tokens."""
+    torch = torch_cuda()
+    say("ffn_tokens repeated slots", T, k, nslots, pattern)
+    d, f = 256, 520
+    slabs = [synth.expert_slab(70 + i, d, f, None) for i in range(nslots)]
+    pool = _pool(torch, slabs, d, f)
+    rng = np.random.default_rng(T * 100 + k)
+    X = rng.standard_normal((T, d)).astype(np.float32)
+    if pattern == "dup":
+        slots = np.array([[1, 1, 1, 1], [1, 1, 2, 2]], np.int32)
+    else:
+        slots = np.zeros((T, k), np.int32)
+    w = rng.random((T, k)).astype(np.float32)
+    y = _run(torch, X, pool, nslots, slots, w, d, f)
+    for t, e in enumerate(_expect(X, slabs, slots, w, d, f, nslots)):
+        assert_close(y[t], e, f"repeated slots t={t} slots={list(slots[t])}")
+
+
 def test_tokens_mixtral_shape_sampled():
     """Full Mixtral expert shape (d 4096, f 14336), 4 tokens top-2 over 4 resident slabs."""
     torch = torch_cuda()
