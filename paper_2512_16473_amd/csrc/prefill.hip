@@ -4,7 +4,8 @@
 //   1. router for all T tokens (the decode router kernel, one block per token);
 //   2. grouping: a stable counting sort of the T*k (token, rank) pairs by expert,
 //      giving per-expert offsets, the sorted pair list and its inverse;
-//   3. hidden states rounded to bf16 for the matrix cores;
+//   3. hidden states rounded to bf16 for the matrix cores (other blocks of the grouping
+//      launch: it does not depend on the routing);
 //   4. grouped GEMM gate/up: for each expert e, H_e = SiLU(X_e W1_e^T) * (X_e W3_e^T),
 //      bf16 MFMA (v_mfma_f32_16x16x32_bf16) with fp32 accumulation, H_e stored bf16; the
 //      tiles of a last, partial round of work groups are split over K, and
@@ -52,9 +53,11 @@ __device__ __forceinline__ uint16_t f2bf(float f)
     return (uint16_t)(u >> 16);
 }
 
-__global__ __launch_bounds__(kThreads) void k_cast_bf16(const float *x, uint16_t *y, int64_t n8)
+// y = bf16(x) over n8 groups of 8 values; `first`, `stride`: this thread's first group
+// and the step between its groups.
+__device__ __forceinline__ void cast_bf16(const float *x, uint16_t *y, int64_t n8, int64_t first, int64_t stride)
 {
-    for (int64_t i = blockIdx.x * (int64_t)kThreads + threadIdx.x; i < n8; i += (int64_t)gridDim.x * kThreads) {
+    for (int64_t i = first; i < n8; i += stride) {
         const float4 a = reinterpret_cast<const float4 *>(x)[2 * i];
         const float4 b = reinterpret_cast<const float4 *>(x)[2 * i + 1];
         uint4 o;
@@ -66,6 +69,8 @@ __global__ __launch_bounds__(kThreads) void k_cast_bf16(const float *x, uint16_t
     }
 }
 
+// Block 0: the grouping below. Blocks 1 ..: the hidden states rounded to bf16 for the
+// matrix cores (independent of the routing, so the two share one launch).
 // Stable counting sort of the pairs p = t*k + r by expert idx[p] (one block).
 // off[e] .. off[e+1] is expert e's range in `perm` (pair ids in increasing order);
 // pos[p] is the place of pair p in that order. The per-expert counts come from LDS
@@ -73,8 +78,14 @@ __global__ __launch_bounds__(kThreads) void k_cast_bf16(const float *x, uint16_t
 // the same expert, counted over the chunk's ids in LDS four at a time.
 constexpr int kGroupThreads = 1024;
 __global__ __launch_bounds__(kGroupThreads) void k_group(const int32_t *idx, int npairs, int n, int32_t *off,
-                                                         int32_t *perm, int32_t *pos)
+                                                         int32_t *perm, int32_t *pos, const float *x, uint16_t *xb,
+                                                         int64_t n8)
 {
+    if (blockIdx.x > 0) {
+        cast_bf16(x, xb, n8, (int64_t)(blockIdx.x - 1) * kGroupThreads + threadIdx.x,
+                  (int64_t)(gridDim.x - 1) * kGroupThreads);
+        return;
+    }
     __shared__ int32_t base[MOE_MAX_EXPERTS];    // counts, then the next free place of each expert
     __shared__ int32_t hist[MOE_MAX_EXPERTS];
     __shared__ uint32_t ids32[kGroupThreads / 4];
@@ -580,11 +591,10 @@ hipError_t launch_prefill(const PrefillPlan &P, const float *X, float *OUT, int3
     if ((e = launch_router(X, P.wr, P.T, P.d, P.n, P.k, idx_d, w_d, s)) != hipSuccess) return e;
     const int npairs = P.T * P.k;
     (void)hipGetLastError();
-    hipLaunchKernelGGL(k_group, dim3(1), dim3(kGroupThreads), 0, s, idx_d, npairs, P.n, ws.off, ws.perm, ws.pos);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
     const int64_t n8 = (int64_t)P.T * P.d / 8;
-    const int cast_blocks = (int)std::min<int64_t>((n8 + kThreads - 1) / kThreads, 4096);
-    hipLaunchKernelGGL(k_cast_bf16, dim3(cast_blocks), dim3(kThreads), 0, s, X, ws.xb, n8);
+    const int cast_blocks = (int)std::min<int64_t>((n8 + kGroupThreads - 1) / kGroupThreads, 1024);
+    hipLaunchKernelGGL(k_group, dim3(1 + cast_blocks), dim3(kGroupThreads), 0, s, idx_d, npairs, P.n, ws.off, ws.perm,
+                       ws.pos, X, ws.xb, n8);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     GemmArgs g{};
