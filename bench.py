@@ -26,6 +26,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 
 def log(*a):
@@ -189,7 +190,8 @@ def host_info():
 
 def host_sweep(moe, wl, world, threads_list=(1, 2, 4, 8, 16)):
     """Host expert path alone: one layer's k experts all missed (the CPU column of the
-    paper's Table III), for several thread counts, nothing else running."""
+    paper's Table III), for several thread counts, nothing else running; both forms of
+    the row dot product (fp32 widening; the AVX512_BF16 pair-dot where the CPU has it)."""
     import numpy as np
     d, f, k = wl.d, wl.f, wl.k
     stride = world["stride"]
@@ -198,16 +200,25 @@ def host_sweep(moe, wl, world, threads_list=(1, 2, 4, 8, 16)):
     x = world["X"][0, 0]
     w = np.full(k, 1.0 / k, np.float32)
     out = {}
-    for t in threads_list:
-        pool = moe.HostPool(t)
-        times = []
-        for _ in range(3):
-            t0 = time.perf_counter()
-            pool.expert_ffn(x, slabs, w, d, f)
-            times.append(time.perf_counter() - t0)
-        pool.close()
-        ms = sorted(times)[1] * 1e3
-        out[str(t)] = {"ms": round(ms, 2), "GB/s": round(k * 3 * d * f * 2 / (ms * 1e-3) / 1e9, 1)}
+    for dot in ("fp32", "bf16"):
+        rows = {}
+        for t in threads_list:
+            pool = moe.HostPool(t)
+            try:
+                pool.set_dot(dot)
+            except moe.MoeError:
+                pool.close()
+                break
+            times = []
+            for _ in range(5):
+                t0 = time.perf_counter()
+                pool.expert_ffn(x, slabs, w, d, f)
+                times.append(time.perf_counter() - t0)
+            pool.close()
+            ms = sorted(times)[2] * 1e3
+            rows[str(t)] = {"ms": round(ms, 2), "GB/s": round(k * 3 * d * f * 2 / (ms * 1e-3) / 1e9, 1)}
+        if rows:
+            out[dot] = rows
     return out
 
 
@@ -402,20 +413,32 @@ def small_batch_study(args, torch, moe, synth, wl):
     }
 
 
-def measured_traffic(args):
-    """HBM bytes per k_gate_up launch from the committed PMC record, if it was taken on
-    the current kernel source and the same workload arguments; else None."""
+def _kernel_record(name):
+    """A committed PMC record (profiles/<name>) if the kernel sources it lists still hash
+    to the value it was taken on; else None."""
     import hashlib
     try:
-        rec = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))
+        rec = json.load(open(os.path.join(ROOT, "profiles", name)))
         # the kernel sources the counters were taken on, hashed in the listed order
         src = b"".join(open(os.path.join(ROOT, f), "rb").read() for f in rec["kernel_sources"])
     except (OSError, ValueError, KeyError, TypeError):
         return None
-    want = {"workload": args.workload, "steps": args.steps, "warmup": args.warmup, "seed": args.seed}
-    if hashlib.sha256(src).hexdigest() != rec.get("kernel_sha256") or rec.get("command_args") != want:
+    if hashlib.sha256(src).hexdigest() != rec.get("kernel_sha256"):
         return None
-    return rec["k_gate_up"]["hbm_bytes_per_launch"]
+    return rec
+
+
+def measured_traffic(args, kernel, bytes_per_launch):
+    """HBM bytes per launch of `kernel` (k_gate_up, k_down) for this run: the ratio of
+    counted (rocprofv3 FETCH_SIZE/WRITE_SIZE, scaled by the copy calibration) to
+    algorithmic bytes per launch in the committed record, taken on the current kernel
+    source with the same workload and seed, times this run's algorithmic bytes per
+    launch. None when no such record exists."""
+    rec = _kernel_record("traffic.json")
+    if rec is None or rec.get("workload") != args.workload or rec.get("seed") != args.seed or kernel not in rec:
+        return None
+    r = rec[kernel]["hbm_bytes_per_launch"] / rec[kernel]["algorithmic_bytes_per_launch"]
+    return {"bytes_per_launch": round(r * bytes_per_launch), "ratio_to_algorithmic": round(r, 4)}
 
 
 def read_stream_yardstick(torch, moe, buf, launch_bytes):
@@ -444,25 +467,55 @@ def read_stream_yardstick(torch, moe, buf, launch_bytes):
     return out
 
 
-def measured_prefill_traffic(args):
-    """HBM bytes per prefill layer (the two grouped GEMMs) from the committed PMC record,
-    if it was taken on the current kernel source with the same workload and seed."""
-    import hashlib
-    try:
-        rec = json.load(open(os.path.join(ROOT, "profiles", "traffic_prefill.json")))
-        src = b"".join(open(os.path.join(ROOT, f), "rb").read() for f in rec["kernel_sources"])
-    except (OSError, ValueError, KeyError, TypeError):
-        return None
-    if (hashlib.sha256(src).hexdigest() != rec.get("kernel_sha256") or rec.get("workload") != args.workload
-            or rec.get("seed") != args.seed):
+def measured_prefill_traffic(d, f, n, k, T):
+    """HBM bytes per prefill layer (the two grouped GEMMs and the gate/up tail combine)
+    from the committed PMC record, if it was taken on the current kernel source at the
+    same layer shape and prompt length."""
+    rec = _kernel_record("traffic_prefill.json")
+    if rec is None or rec.get("shape") != {"d": d, "f": f, "n": n, "k": k, "T": T}:
         return None
     return rec["hbm_bytes_per_layer"]
+
+
+def prefill_pass(torch, moe, pool, wr, X, d, f, n, k, L, warmup, steps):
+    """Prompt X [T, d] through layers 0..L-1 per step (layer l: slabs l*n .. l*n+n-1 of
+    pool, router wr[l]), every expert resident; `warmup` untimed and `steps` timed steps.
+    Time from events on the stream the library launches on (torch's current stream)."""
+    T = X.shape[0]
+    stride = moe.slab_bytes(d, f)
+    out = torch.empty((T, d), device="cuda")
+    ws = torch.empty(moe.prefill_workspace_bytes(d, f, n, k, T), dtype=torch.uint8, device="cuda")
+
+    def step():
+        for l in range(L):
+            moe.prefill_forward(X, wr[l], pool[l * n * stride:(l + 1) * n * stride], d, f, n, k, out, ws)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t1 = time.perf_counter()
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t1
+    per_layer_us = e0.elapsed_time(e1) * 1e3 / (steps * L)
+    bytes_layer = n * 3 * d * f * 2.0
+    flops_layer = 2.0 * 3 * d * f * T * k
+    hbm = bytes_layer / (per_layer_us * 1e-6) / 1e9
+    tf = flops_layer / (per_layer_us * 1e-6) / 1e12
+    return {"tokens_per_s": round(T * steps / wall, 1), "ms_per_prompt": round(wall / steps * 1e3, 3),
+            "us_per_layer": round(per_layer_us, 2), "hbm_gbs": round(hbm, 1),
+            "hbm_frac": round(hbm / HBM_PEAK_GBS, 4), "mfma_tflops": round(tf, 1),
+            "mfma_frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
+            "traffic_bytes_per_layer": measured_prefill_traffic(d, f, n, k, T)}
 
 
 def bench_prefill(args, torch, moe, synth, wl):
     """One prompt of wl.T tokens through every layer, all experts resident in HBM
     (L x n slabs, layers visited in order so no slab is reused while cached)."""
-    import numpy as np
     d, f, n, k, L, T = wl.d, wl.f, wl.n, wl.k, wl.L, wl.T
     stride = moe.slab_bytes(d, f)
     t0 = time.perf_counter()
@@ -475,52 +528,99 @@ def bench_prefill(args, torch, moe, synth, wl):
     wr = torch.stack([synth.router_weights_torch(synth.seed_for(args.seed, wl.name, "router", l), n, d)
                       for l in range(L)]).contiguous()
     X = torch.from_numpy(synth.iid_states(synth.seed_for(args.seed, wl.name, "prompt"), T, d)).cuda()
-    out = torch.empty((T, d), device="cuda")
-    ws = torch.empty(moe.prefill_workspace_bytes(d, f, n, k, T), dtype=torch.uint8, device="cuda")
     torch.cuda.synchronize()
     log(f"prefill world ready in {time.perf_counter() - t0:.1f}s ({pool.numel() / 1e9:.1f} GB of experts in HBM)")
-
-    def step():
-        for l in range(L):
-            moe.prefill_forward(X, wr[l], pool[l * n * stride:(l + 1) * n * stride], d, f, n, k, out, ws)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t1 = time.perf_counter()
-    e0.record()
-    for _ in range(args.steps):
-        step()
-    e1.record()
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t1
-    ms = e0.elapsed_time(e1)
-    per_layer_us = ms * 1e3 / (args.steps * L)
-    bytes_layer = n * 3 * d * f * 2.0
-    flops_layer = 2.0 * 3 * d * f * T * k
-    hbm = bytes_layer / (per_layer_us * 1e-6) / 1e9
-    tf = flops_layer / (per_layer_us * 1e-6) / 1e12
+    r = prefill_pass(torch, moe, pool, wr, X, d, f, n, k, L, args.warmup, args.steps)
     return {
         "metric": "prefill MoE-layer tokens/s + achieved HBM GB/s (%peak), Mixtral-8x7B shape",
-        "value": round(T * args.steps / wall, 1),
+        "value": r["tokens_per_s"],
         "unit": "tokens/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(wall / args.steps * 1e3, 3),
+        "ms_per_step": r["ms_per_prompt"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": wl.desc, "d_model": d, "d_ffn": f, "experts": n, "top_k": k, "layers": L,
                    "prompt_tokens": T, "weights": "bf16, activations rounded to bf16, fp32 accumulate",
                    "parallelism": "single GPU"},
         "roofline": {"kernel": "prefill layer (router, grouping, grouped MFMA GEMMs, combine)", "bound": "hbm",
-                     "achieved": round(hbm, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(hbm / HBM_PEAK_GBS, 4), "traffic": measured_prefill_traffic(args),
+                     "achieved": r["hbm_gbs"], "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": r["hbm_frac"], "traffic": r["traffic_bytes_per_layer"],
                      "traffic_unit": "HBM bytes per layer of the grouped GEMMs (rocprofv3 FETCH_SIZE x2.0 + "
                                      "WRITE_SIZE, profiles/traffic_prefill.json)",
-                     "mfma_tflops": round(tf, 1), "mfma_peak_tflops": 2500.0, "mfma_frac": round(tf / 2500.0, 4),
-                     "us_per_layer": round(per_layer_us, 2)},
+                     "mfma_tflops": r["mfma_tflops"], "mfma_peak_tflops": MFMA_BF16_PEAK_TFLOPS,
+                     "mfma_frac": r["mfma_frac"], "us_per_layer": r["us_per_layer"]},
         "cpu_baseline": None,
     }
+
+
+def all_resident_and_prefill(args, torch, moe, synth, wl, world, xd, tokens=64, prompts=4):
+    """The GPU-bound regime on the same weights: every expert of every layer resident
+    (a static cache holding all n experts; MI355X's HBM holds a Mixtral-sized expert set),
+    so each decode token runs router + hit FFN + reduce per layer with no host work and
+    no copies. Timed once with the kernel timing events off (tokens/s) and once with
+    them on (kernel rooflines). Then a 512-token prompt through the same resident
+    layers (prefill: batched router, grouping, grouped MFMA GEMMs)."""
+    d, f, n, k, L = wl.d, wl.f, wl.n, wl.k, wl.L
+    stride = world["stride"]
+    H = world["H"]
+    host_addrs = [world["hosts"][l % H].ptr + e * stride for l in range(L) for e in range(n)]
+    content = [list(range(n)) for _ in range(L)]
+    pool = torch.empty(L * n * stride, dtype=torch.uint8, device="cuda")
+    t0 = time.perf_counter()
+    cache = moe.Cache(L, n, n, k, policy="static", static_content=content)
+    rt = moe.Runtime(d, f, n, k, n, L, world["wr"], pool, host_addrs, cache, world["hp"])   # loads every slab
+    torch.cuda.synchronize()
+    log(f"all-resident world: {pool.numel() / 1e9:.1f} GB of experts loaded in {time.perf_counter() - t0:.1f}s")
+    streams = (torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream())
+    out = torch.empty((2, L, d), dtype=torch.float32, device="cuda")
+    T = xd.shape[0]
+
+    def run(t0_, count):
+        for t in range(t0_, t0_ + count):
+            rt.decode_step(xd[t % T], out[t % 2], streams)
+        torch.cuda.synchronize()
+
+    run(0, 4)
+    rt.reset_stats()
+    t1 = time.perf_counter()
+    run(4, tokens)
+    dt = time.perf_counter() - t1
+    st = rt.stats()
+    assert st["expert_misses"] == 0 and st["fills"] == 0
+    rt.set_timing(True)
+    run(4, tokens)
+    st = rt.stats()
+    rt.set_timing(False)
+    rt.close()
+    cache.close()
+    alg_layer = k * 3 * d * f * 2 + n * d * 4
+    us_layer = dt / (tokens * L) * 1e6
+    gu = st["gate_up_bytes"] / (st["gate_up_ms"] * 1e-3) / 1e9
+    dn = st["down_bytes"] / (st["down_ms"] * 1e-3) / 1e9
+    res = {
+        "what": f"every expert resident (static cache of all {n} experts per layer, no misses, no copies); "
+                f"{tokens} tokens after 4 warm-up, timing events off; kernel figures from a second pass of "
+                f"the same tokens with events on",
+        "tokens_per_s": round(tokens / dt, 2), "ms_per_token": round(dt / tokens * 1e3, 3),
+        "us_per_layer": round(us_layer, 2),
+        "hbm_floor_us_per_layer": round(alg_layer / (HBM_PEAK_GBS * 1e3), 2),
+        "frac_of_floor": round(alg_layer / (HBM_PEAK_GBS * 1e3) / us_layer, 4),
+        "k_gate_up": {"avg_us": round(st["gate_up_ms"] / st["gate_up_launches"] * 1e3, 2),
+                      "gbs": round(gu, 1), "frac": round(gu / HBM_PEAK_GBS, 4)},
+        "k_down": {"avg_us": round(st["down_ms"] / st["down_launches"] * 1e3, 2),
+                   "gbs": round(dn, 1), "frac": round(dn / HBM_PEAK_GBS, 4)},
+        "hit_ffn_us_per_layer": round((st["gate_up_ms"] + st["down_ms"]) / st["gate_up_launches"] * 1e3, 2),
+    }
+    log(json.dumps(res))
+    X = torch.from_numpy(synth.iid_states(synth.seed_for(args.seed, "prefill", "prompt"), 512, d)).cuda()
+    pf = prefill_pass(torch, moe, pool, world["wr"], X, d, f, n, k, L, 2, prompts)
+    pf["what"] = (f"one 512-token prompt (i.i.d. N(0,1)) through the {L} resident layers; 2 warm-up + {prompts} "
+                  f"timed prompts; HBM fraction on the {n} expert slabs per layer, MFMA fraction of the bf16 "
+                  f"dense peak")
+    log(json.dumps(pf))
+    del pool
+    torch.cuda.empty_cache()
+    return res, pf
 
 
 def moe_slab_bytes(d, f):
@@ -536,9 +636,13 @@ def main():
     ap.add_argument("--workload", default="mixtral", choices=["mixtral", "phi", "fine", "tiny", "prefill"])
     ap.add_argument("--threads", type=int, default=0, help="host expert threads (0: OMP_NUM_THREADS or all cores)")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--host-dot", default="auto", choices=["auto", "fp32", "bf16"],
+                    help="form of the host path's dot products (bf16: AVX512_BF16 pair-dot)")
     ap.add_argument("--pinned-gb", type=float, default=56.0, help="page-locked host memory for expert copies (GiB)")
     ap.add_argument("--cpu-baseline-s", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-resident", action="store_true",
+                    help="skip the all-resident decode and prefill sub-measurements of the Mixtral line")
     ap.add_argument("--policy", default="lru", choices=["lru", "fifo", "static"],
                     help="cache replacement policy (Section IV-D; the paper's is LRU)")
     ap.add_argument("--ways", type=int, default=0,
@@ -596,6 +700,7 @@ def main():
     world = build_world(torch, moe, synth, wl, steps_total, args.seed, args.threads, args.pinned_gb,
                         policy=args.policy, budget_gb=args.budget_gb, ways=args.ways or None)
     rt, xd = world["rt"], world["xd"]
+    world["hp"].set_dot(args.host_dot)
     rt.set_fill_limit(args.fill_limit)
     rt.set_nonblocking(args.nonblocking)
     L, k, d = wl.L, wl.k, wl.d
@@ -648,7 +753,7 @@ def main():
             "d_model": wl.d, "d_ffn": wl.f, "experts": wl.n, "top_k": wl.k, "layers": wl.L,
             "cache_ways": args.ways or wl.ways, "shared_d_ffn": wl.f_shared, "batch": 1,
             "weights": "bf16, fp32 accumulate", "cache_start": f"cold, {args.warmup} warmup tokens",
-            "host_threads": world["hp"].threads, "parallelism": "single GPU",
+            "host_threads": world["hp"].threads, "host_dot": world["hp"].dot, "parallelism": "single GPU",
             "host_expert_layers_distinct": world["H"],
             "cache_policy": world["policy"], "covered_layers": world["covered"],
             "post_fetch": (f"at most {args.fill_limit} slabs in flight" if args.fill_limit
@@ -662,8 +767,10 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(gu_gbs / HBM_PEAK_GBS, 4),
-            "traffic": measured_traffic(args),
-            "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE x2.0 + WRITE_SIZE, profiles/traffic.json)",
+            "traffic": None,
+            "traffic_unit": "HBM bytes per launch: this run's algorithmic bytes per launch x the counted/algorithmic "
+                            "ratio of rocprofv3 FETCH_SIZE x2.0 + WRITE_SIZE on the same kernel source, workload "
+                            "and seed (profiles/traffic.json)",
             "launches": st["gate_up_launches"],
             "avg_us": round(st["gate_up_ms"] / max(1, st["gate_up_launches"]) * 1e3, 2),
             "bytes_per_launch": round(st["gate_up_bytes"] / max(1, st["gate_up_launches"])),
@@ -685,6 +792,15 @@ def main():
             "inflight_misses_per_token": round(st["inflight_misses"] / K, 3),
         },
     }
+    for kern, key in (("k_gate_up", "roofline"), ("k_down", "hit_ffn")):
+        bpl = (st["gate_up_bytes"] / max(1, st["gate_up_launches"]) if kern == "k_gate_up"
+               else st["down_bytes"] / max(1, st["down_launches"]))
+        tr = measured_traffic(args, kern, bpl)
+        if kern == "k_gate_up":
+            result["roofline"]["traffic"] = None if tr is None else tr["bytes_per_launch"]
+            result["roofline"]["traffic_ratio"] = None if tr is None else tr["ratio_to_algorithmic"]
+        else:
+            result["hit_ffn"]["down_traffic_ratio"] = None if tr is None else tr["ratio_to_algorithmic"]
     log(json.dumps(result["trace"]), json.dumps(result["hit_ffn"]))
     if world["pool"] is not None and st["gate_up_launches"]:
         ys = read_stream_yardstick(torch, moe, world["pool"], result["roofline"]["bytes_per_launch"])
@@ -723,6 +839,9 @@ def main():
             "host_ffn_ms_per_token": round(s2["host_ffn_ms"] / K, 3)}
         log(json.dumps(result["bounded_post_fetch"]))
         rt = rt2
+    if args.workload == "mixtral" and not args.no_resident:
+        rt.close()
+        result["all_resident"], result["prefill"] = all_resident_and_prefill(args, torch, moe, synth, wl, world, xd)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, world, args.seed, args.cpu_baseline_s, args.warmup)
     else:

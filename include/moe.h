@@ -7,7 +7,7 @@
  * selected experts in a per-layer set-associative GPU expert cache with LRU
  * eviction, the SwiGLU FFN of cache-hit experts on the GPU, the FFN of missed
  * experts on a host thread pool, asynchronous post-fetch of missed experts into
- * the cache for future tokens, and the weighted combine (Section III-A steps 1-3,
+ * the cache for later tokens, and the weighted combine (Section III-A steps 1-3,
  * Section III-B cache design, Section III-C copy streams). A batched prefill path
  * (all experts resident, grouped by expert, MFMA GEMMs) is also exported.
  *
@@ -147,7 +147,11 @@ int moe_cache_update(moe_cache *c, int layer, const int32_t *experts, int k,
  */
 int moe_cache_update_masked(moe_cache *c, int layer, const int32_t *experts, int k,
                             const uint8_t *insert, int32_t *fill_slot_out, int32_t *evicted_out);
-/* Expert -> slot table of one layer: host [n], -1 for experts not cached. */
+/*
+ * Expert -> slot table of one layer: host [n], -1 for experts not cached. (The device
+ * [L][n] mirror that the hit kernels read belongs to the runtime, which installs a row
+ * only once its post-fetch copies have landed; moe_runtime_device_slotmap reads it.)
+ */
 int moe_cache_slotmap(const moe_cache *c, int layer, int32_t *slotmap_out);
 /*
  * Checkpoint and resume of the cache state (every set's slot contents, their recency
@@ -232,10 +236,29 @@ int moe_host_pool_create(int n_threads, moe_host_pool **out);
 void moe_host_pool_destroy(moe_host_pool *p);
 int moe_host_pool_threads(const moe_host_pool *p);
 /*
+ * Form of the host path's row dot products (the Table III CPU study on this host):
+ *   MOE_HOST_DOT_FP32  bf16 weights widened to fp32, fp32 FMAs (AVX-512F when the CPU
+ *                      has it, else scalar). The default.
+ *   MOE_HOST_DOT_BF16  the AVX512_BF16 pair-dot instruction (exact bf16 x bf16 products,
+ *                      fp32 sums); x and h are each split into two bf16 parts hi + lo with
+ *                      |v - hi - lo| <= 2^-18 |v|, so results stay at fp32-accumulation
+ *                      error. MOE_EINVAL on a CPU without AVX512_BF16.
+ *   MOE_HOST_DOT_AUTO  the default form.
+ * Either way each output row is one thread's fixed-order sum. moe_host_pool_get_dot
+ * returns the form in use (FP32 or BF16), or MOE_EINVAL for a null handle.
+ */
+#define MOE_HOST_DOT_AUTO 0
+#define MOE_HOST_DOT_FP32 1
+#define MOE_HOST_DOT_BF16 2
+int moe_host_pool_set_dot(moe_host_pool *p, int kind);
+int moe_host_pool_get_dot(const moe_host_pool *p);
+/*
  * y = sum_j w[j] * FFN(slabs[j], x), all host memory: x fp32 [d], slabs[j] bf16
  * slab pointers, w fp32 [n_experts], y fp32 [d] (overwritten). Rows are split
  * across the pool's threads; each row is one thread's fixed-order sum, so the
  * result does not depend on the thread count. 0 <= n_experts <= MOE_MAX_TOPK.
+ * A pool serves one call at a time: calls that overlap (from several threads, or
+ * several runtimes sharing the pool) are serialised.
  */
 int moe_host_expert_ffn(moe_host_pool *p, const float *x, const void *const *slabs,
                         const float *w, int n_experts, int d, int f, float *y);
@@ -384,7 +407,10 @@ size_t moe_prefill_workspace_bytes(const moe_prefill_desc *P, int T);
  * OUT[t] = sum_j w[t][j] FFN_{idx[t][j]}(X[t]) for t < T.
  * X_dev device fp32 [T][d]; OUT_dev device fp32 [T][d]; idx_dev/w_dev device
  * [T][k] routing outputs (nullable). Activations are rounded to bf16 for the
- * matrix cores; accumulation is fp32.
+ * matrix cores; accumulation is fp32. The workspace (device, 256-byte aligned,
+ * >= moe_prefill_workspace_bytes(P, T)) holds the grouping and the intermediate
+ * activations, so the call allocates nothing. d and f must be multiples of 128
+ * (d <= MOE_MAX_D); MOE_EINVAL otherwise; T == 0 is a no-op.
  */
 int moe_prefill_forward(const moe_prefill_desc *P, const float *X_dev, int T, float *OUT_dev,
                         int32_t *idx_dev, float *w_dev, void *workspace, size_t workspace_bytes,

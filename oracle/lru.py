@@ -4,8 +4,8 @@ Section III-A/B of the paper: GPU memory holds an N-index, M-way set-associative
 expert cache whose index is the layer number; each set keeps up to M experts of
 its layer and evicts with LRU. On each access (one token at one layer) the cache
 is checked for the selected experts (step 1), hits run on the GPU and misses on
-the CPU (step 2), and every missed expert is then copied into the cache for
-future tokens (step 3).
+the CPU (step 2), and every missed expert is then copied into the cache so
+later tokens hit it (step 3).
 
 Points the paper leaves open, and the reading taken here:
   * hits are decided for all selected experts against the state before the token;

@@ -229,6 +229,16 @@ class HostPool:
     def threads(self):
         return int(_lib.moe_host_pool_threads(self.handle))
 
+    @property
+    def dot(self):
+        """Form of the row dot products: "fp32" (widened weights) or "bf16" (pair-dot)."""
+        v = int(_lib.moe_host_pool_get_dot(self.handle))
+        return {1: "fp32", 2: "bf16"}[v]
+
+    def set_dot(self, kind):
+        """kind: "auto", "fp32" or "bf16" (MoeError if the CPU lacks AVX512_BF16)."""
+        _check("moe_host_pool_set_dot", _lib.moe_host_pool_set_dot(self.handle, _abi.HOST_DOT[kind]))
+
     def close(self):
         if getattr(self, "handle", None) and _lib is not None:
             _lib.moe_host_pool_destroy(self.handle)

@@ -16,6 +16,7 @@ c_char_p = ctypes.c_char_p
 
 MOE_OK, MOE_EINVAL, MOE_EHIP, MOE_ESTATE, MOE_ENOMEM = 0, -1, -2, -3, -4
 MAX_EXPERTS, MAX_TOPK, MAX_D, MAX_TOKENS = 256, 16, 8192, 8
+HOST_DOT = {"auto": 0, "fp32": 1, "bf16": 2}
 
 
 class LayerDesc(ctypes.Structure):
@@ -74,6 +75,8 @@ SIGNATURES = [
     ("moe_host_pool_create", c_int, [c_int, ctypes.POINTER(c_void_p)]),
     ("moe_host_pool_destroy", None, [c_void_p]),
     ("moe_host_pool_threads", c_int, [c_void_p]),
+    ("moe_host_pool_set_dot", c_int, [c_void_p, c_int]),
+    ("moe_host_pool_get_dot", c_int, [c_void_p]),
     ("moe_host_expert_ffn", c_int, [c_void_p, c_f32p, ctypes.POINTER(c_void_p), c_f32p, c_int, c_int, c_int,
                                     c_f32p]),
     ("moe_runtime_create", c_int, [ctypes.POINTER(LayerDesc), ctypes.POINTER(c_void_p)]),

@@ -56,24 +56,30 @@ size_t moe_ffn_workspace_bytes(int max_jobs, int d, int f_max)
     return moe::ffn_workspace_bytes(max_jobs, d, f_max);
 }
 
-int moe_expert_ffn_hits(const float *x, const void *slot_pool, int n_slots, const int32_t *hit_slots,
-                        const float *hit_w, int n_hits, int d, int f, float *y, void *workspace,
-                        size_t workspace_bytes, void *stream)
+}  // extern "C"
+
+namespace {
+
+// Argument checks shared by the two hit-FFN entry points (workspace aside).
+int check_ffn_hits(const char *fn, const float *x, const void *slot_pool, int n_slots, const int32_t *hit_slots,
+                   const float *hit_w, int n_hits, int d, int f, float *y)
 {
-    MOE_GUARD_BEGIN
-    MOE_REQUIRE(n_hits >= 0 && n_hits <= MOE_MAX_TOPK, "moe_expert_ffn_hits: n_hits=%d out of [0,%d]", n_hits,
-                MOE_MAX_TOPK);
-    MOE_REQUIRE(d > 0 && d % 8 == 0 && d <= MOE_MAX_D, "moe_expert_ffn_hits: d=%d must be a multiple of 8 in [8,%d]",
-                d, MOE_MAX_D);
-    MOE_REQUIRE(f > 0 && f % 8 == 0, "moe_expert_ffn_hits: f=%d must be a positive multiple of 8", f);
-    MOE_REQUIRE(x && y && workspace, "moe_expert_ffn_hits: null pointer");
-    MOE_REQUIRE(n_slots >= 0, "moe_expert_ffn_hits: n_slots=%d < 0", n_slots);
-    MOE_REQUIRE(n_hits == 0 || (slot_pool && hit_slots && hit_w), "moe_expert_ffn_hits: null pointer");
+    MOE_REQUIRE(n_hits >= 0 && n_hits <= MOE_MAX_TOPK, "%s: n_hits=%d out of [0,%d]", fn, n_hits, MOE_MAX_TOPK);
+    MOE_REQUIRE(d > 0 && d % 8 == 0 && d <= MOE_MAX_D, "%s: d=%d must be a multiple of 8 in [8,%d]", fn, d,
+                MOE_MAX_D);
+    MOE_REQUIRE(f > 0 && f % 8 == 0, "%s: f=%d must be a positive multiple of 8", fn, f);
+    MOE_REQUIRE(x && y, "%s: null pointer", fn);
+    MOE_REQUIRE(n_slots >= 0, "%s: n_slots=%d < 0", fn, n_slots);
+    MOE_REQUIRE(n_hits == 0 || (slot_pool && hit_slots && hit_w), "%s: null pointer", fn);
     MOE_REQUIRE(moe::aligned16(x) && moe::aligned16(y) && moe::aligned16(slot_pool),
-                "moe_expert_ffn_hits: x/y/slot_pool not 16-byte aligned");
-    MOE_REQUIRE(((uintptr_t)workspace & 255u) == 0, "moe_expert_ffn_hits: workspace not 256-byte aligned");
-    const size_t need = moe::ffn_workspace_bytes(n_hits, d, f);
-    MOE_REQUIRE(workspace_bytes >= need, "moe_expert_ffn_hits: workspace %zu < %zu bytes", workspace_bytes, need);
+                "%s: x/y/slot_pool not 16-byte aligned", fn);
+    return MOE_OK;
+}
+
+// gate/up, down and reduce of the hit experts over a bound workspace.
+int run_ffn_hits(const float *x, const void *slot_pool, int n_slots, const int32_t *hit_slots, const float *hit_w,
+                 int n_hits, int d, int f, float *y, void *workspace, void *stream)
+{
     moe::FfnParams p{};
     p.x = x;
     p.pool = static_cast<const uint8_t *>(slot_pool);
@@ -93,6 +99,24 @@ int moe_expert_ffn_hits(const float *x, const void *slot_pool, int n_slots, cons
     MOE_HIP(moe::launch_ffn_stream(p, s, nullptr, nullptr));
     MOE_HIP(moe::launch_ffn_reduce(p, nullptr, y, s));
     return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int moe_expert_ffn_hits(const float *x, const void *slot_pool, int n_slots, const int32_t *hit_slots,
+                        const float *hit_w, int n_hits, int d, int f, float *y, void *workspace,
+                        size_t workspace_bytes, void *stream)
+{
+    MOE_GUARD_BEGIN
+    int rc = check_ffn_hits("moe_expert_ffn_hits", x, slot_pool, n_slots, hit_slots, hit_w, n_hits, d, f, y);
+    if (rc != MOE_OK) return rc;
+    MOE_REQUIRE(workspace, "moe_expert_ffn_hits: null workspace");
+    MOE_REQUIRE(((uintptr_t)workspace & 255u) == 0, "moe_expert_ffn_hits: workspace not 256-byte aligned");
+    const size_t need = moe::ffn_workspace_bytes(n_hits, d, f);
+    MOE_REQUIRE(workspace_bytes >= need, "moe_expert_ffn_hits: workspace %zu < %zu bytes", workspace_bytes, need);
+    return run_ffn_hits(x, slot_pool, n_slots, hit_slots, hit_w, n_hits, d, f, y, workspace, stream);
     MOE_GUARD_END
 }
 

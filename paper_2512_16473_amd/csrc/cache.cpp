@@ -1,6 +1,6 @@
 // Host-side slot table of the N-index, M-way expert cache (Section III-B):
-// one set per covered layer, LRU replacement with every missed expert inserted for
-// future tokens (Section III-A step 3). Section IV-D's comparison policies are also
+// one set per covered layer, LRU replacement with every missed expert inserted so that
+// later tokens hit it (Section III-A step 3). Section IV-D's comparison policies are also
 // here: FIFO (a hit does not refresh its slot) and static (a fixed content, misses
 // never inserted).
 #include <algorithm>

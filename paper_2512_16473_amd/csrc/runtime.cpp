@@ -3,7 +3,7 @@
 //   step 1  cache check of the selected experts in the layer's set;
 //   step 2a cache hits computed on the GPU from their cache slots;
 //   step 2b the hidden state copied to the host, missed experts computed there;
-//   step 3  missed experts' weights copied into the cache for future tokens
+//   step 3  missed experts' weights copied into the cache so later tokens find them there
 //           (post-fetch), on a stream of its own (Section III-C keeps weight copies
 //           off the stream that carries activations).
 //

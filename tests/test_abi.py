@@ -109,7 +109,8 @@ def _lib_trace(seq, n, ways, k):
     return out, c
 
 
-@pytest.mark.parametrize("k,ways,length", [(1, 2, 6), (1, 3, 6), (2, 2, 5), (2, 3, 5), (2, 4, 4)])
+@pytest.mark.parametrize("k,ways,length", [(1, 1, 6), (1, 2, 6), (1, 3, 6), (1, 4, 6),
+                                           (2, 2, 6), (2, 3, 6), (2, 4, 6)])
 def test_library_lru_exhaustive_vs_oracle(k, ways, length):
     n = 4
     subs = [list(c) for c in itertools.combinations(range(n), k)]
@@ -313,10 +314,30 @@ def _pool_case(d, f, ne, seed):
     return x, slabs, w
 
 
-@pytest.mark.parametrize("d,f,ne", [(256, 512, 2), (64, 40, 3), (512, 1024, 1), (128, 96, 8)])
-def test_host_expert_path_vs_oracle(d, f, ne):
+def _cpu_flags():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("flags"):
+                    return set(line.split(":", 1)[1].split())
+    except OSError:
+        pass
+    return set()
+
+
+_HOST_DOTS = ["fp32"] + (["bf16"] if "avx512_bf16" in _cpu_flags() else [])
+
+
+@pytest.mark.parametrize("dot", _HOST_DOTS)
+@pytest.mark.parametrize("d,f,ne", [(256, 512, 2), (64, 40, 3), (512, 1024, 1), (128, 96, 8), (4096, 136, 2)])
+def test_host_expert_path_vs_oracle(d, f, ne, dot):
+    """Both forms of the host dot product (fp32 widening; AVX512_BF16 pair-dot with
+    hi + lo activation parts) against the oracle, at fp32-accumulation error; f = 40,
+    96, 136 leave 8, 0 and 8 elements past a 32-wide step (the masked tail)."""
     x, slabs, w = _pool_case(d, f, ne, 40 + d + ne)
     pool = moe.HostPool(4)
+    pool.set_dot(dot)
+    assert pool.dot == dot
     y = pool.expert_ffn(x, slabs, w, d, f)
     ys = np.stack([oracle.expert(x, s, d, f) for s in slabs])
     ref = oracle.combine(ys, w)
@@ -325,13 +346,56 @@ def test_host_expert_path_vs_oracle(d, f, ne):
     assert err <= 1e-4 * rms, (err, rms)
 
 
-def test_host_expert_path_thread_independent_and_empty():
+@pytest.mark.parametrize("dot", _HOST_DOTS)
+def test_host_expert_path_thread_independent_and_empty(dot):
     d, f = 256, 512
     x, slabs, w = _pool_case(d, f, 2, 5)
-    y1 = moe.HostPool(1).expert_ffn(x, slabs, w, d, f)
-    y5 = moe.HostPool(5).expert_ffn(x, slabs, w, d, f)
+    p1, p5 = moe.HostPool(1), moe.HostPool(5)
+    p1.set_dot(dot)
+    p5.set_dot(dot)
+    y1 = p1.expert_ffn(x, slabs, w, d, f)
+    y5 = p5.expert_ffn(x, slabs, w, d, f)
     assert np.array_equal(y1, y5)
     y0 = moe.HostPool(3).expert_ffn(x, [], np.zeros(0, np.float32), d, f, y=np.full(d, 7.0, np.float32))
     assert np.all(y0 == 0)
     with pytest.raises(moe.MoeError):
         moe.HostPool(2).expert_ffn(x, slabs, w, 250, f)
+
+
+def test_host_pool_dot_kinds_and_shared_use():
+    """The dot-form switch (unknown kinds refused; bf16 refused without AVX512_BF16),
+    and one pool used from several threads at once: calls are serialised, so every
+    result equals the one-call result."""
+    import threading
+    p = moe.HostPool(3)
+    assert p.dot == "fp32"
+    p.set_dot("auto")
+    assert p.dot == "fp32"
+    with pytest.raises(KeyError):
+        p.set_dot("fp8")
+    assert _abi_lib().moe_host_pool_set_dot(p.handle, 7) == -1
+    if "bf16" not in _HOST_DOTS:
+        with pytest.raises(moe.MoeError):
+            p.set_dot("bf16")
+    d, f = 128, 96
+    cases = [_pool_case(d, f, 2, 70 + i) for i in range(6)]
+    want = [p.expert_ffn(x, s, w, d, f) for x, s, w in cases]
+    got = [None] * len(cases)
+
+    def work(i):
+        for _ in range(20):
+            x, s, w = cases[i]
+            got[i] = p.expert_ffn(x, s, w, d, f)
+
+    th = [threading.Thread(target=work, args=(i,)) for i in range(len(cases))]
+    for t in th:
+        t.start()
+    for t in th:
+        t.join()
+    for a, b in zip(got, want):
+        assert np.array_equal(a, b)
+
+
+def _abi_lib():
+    from paper_2512_16473_amd import _lib
+    return _lib

@@ -97,15 +97,38 @@ def test_hits_parity_full_shape(name):
 
 
 def test_combine():
+    """moe_combine against the oracle's combine (Section I: the layer output is the
+    gate-weighted sum of the selected experts' outputs, a shared expert at weight 1).
+    The GPU hit part and the host miss part each arrive already weighted; their sum
+    plus the shared expert must equal the oracle's combine over all selected experts."""
     torch = torch_cuda()
     import paper_2512_16473_amd as moe
     say("combine")
-    d = 1000
-    a, b, c = (torch.randn(d, device="cuda") for _ in range(3))
-    out = torch.empty(d, device="cuda")
-    moe.combine(out, a, b, c)
-    assert torch.equal(out, (a + b) + c)
-    moe.combine(out, None, b, None)
-    assert torch.equal(out, b)
+    d, f, n, k = 264, 520, 6, 4
+    slabs = [synth.expert_slab(1200 + e, d, f, None) for e in range(n)]
+    shared = synth.expert_slab(1299, d, 2 * f, None)
+    rng = np.random.default_rng(11)
+    x = rng.standard_normal(d).astype(np.float32)
+    sel = [4, 1, 5, 0]
+    w = rng.random(k).astype(np.float32)
+    w /= w.sum()
+    ys = np.stack([oracle.expert(x, slabs[e], d, f) for e in sel])
+    y_sh = oracle.expert(x, shared, d, 2 * f)
+    hits, misses = [0, 2], [1, 3]                  # ranks that ran on the GPU / on the host
+    y_gpu = oracle.combine(ys[hits], w[hits])
+    y_host = oracle.combine(ys[misses], w[misses])
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda()
+    out = torch.full((d,), float("nan"), device="cuda")
+    moe.combine(out, dev(y_gpu), dev(y_host), dev(y_sh))
+    torch.cuda.synchronize()
+    r = assert_close(out.cpu().numpy(), oracle.combine(ys, w, y_shared=y_sh), "combine, hits + misses + shared")
+    # every hit (no host part, no shared expert) and every miss (no GPU part)
+    moe.combine(out, dev(oracle.combine(ys, w)), None, None)
+    torch.cuda.synchronize()
+    assert_close(out.cpu().numpy(), oracle.combine(ys, w), "combine, all hits")
+    moe.combine(out, None, dev(oracle.combine(ys, w)), dev(y_sh))
+    torch.cuda.synchronize()
+    assert_close(out.cpu().numpy(), oracle.combine(ys, w, y_shared=y_sh), "combine, all misses + shared")
     moe.combine(out)
-    assert torch.count_nonzero(out) == 0
+    assert torch.count_nonzero(out) == 0            # nothing selected: zero output
+    say("  max|err|/RMS", r)

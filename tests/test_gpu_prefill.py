@@ -87,8 +87,10 @@ def test_prefill_small(d, f, n, k, T):
 
 
 def test_prefill_mixtral_full_shape():
-    """Config: Mixtral-8x7B-shaped prefill, one 512-token prompt, all 8 experts resident;
-    every token's routing checked, outputs of a sample of tokens compared."""
+    """Config: Mixtral-8x7B-shaped prefill, one 512-token prompt, all 8 experts resident,
+    in the launch configuration the benchmark times (one M tile per expert, the gate/up
+    tail split over K on 8 XCDs): every token's routing and every token's output
+    compared with the oracle."""
     torch = torch_cuda()
     import paper_2512_16473_amd as moe
     wl = synth.WORKLOADS["prefill"]
@@ -112,11 +114,13 @@ def test_prefill_mixtral_full_shape():
     counts = np.bincount(idx.ravel(), minlength=n)
     say("  tokens per expert", counts.tolist())
     worst = 0.0
-    for t in list(range(0, T, 37)) + [T - 1]:
+    for t in range(T):
         _, _, ref, _ = oracle.moe_token(X[t], wr, host, k, f, forced_set=sets[t])
         r = rel_err(out[t], ref)
         assert r <= TOL, (t, r)
         worst = max(worst, r)
+        if t % 128 == 127:
+            say("  tokens compared", t + 1, "worst max|err|/RMS so far", worst)
     say("  worst max|err|/RMS", worst)
 
 

@@ -26,7 +26,7 @@ def _run(seq, ways):
 
 
 @pytest.mark.parametrize("k,ways,length", [(1, 1, 6), (1, 2, 6), (1, 3, 6), (1, 4, 6),
-                                           (2, 2, 5), (2, 3, 5), (2, 4, 5)])
+                                           (2, 2, 6), (2, 3, 6), (2, 4, 6)])
 def test_exhaustive_vs_definitional(k, ways, length):
     n = 4
     subs = _subsets(n, k)
