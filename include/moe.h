@@ -189,6 +189,22 @@ int moe_expert_ffn_hits(const float *x, const void *slot_pool, int n_slots, cons
                         void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * moe_expert_ffn_hits without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc). Same arguments, kernels and results as moe_expert_ffn_hits; the
+ * job header, h and the split-K partials live in a library-owned static device array
+ * of moe_ffn_noalloc_max_bytes() bytes (8 MiB), one per device, held until the process
+ * ends. The call allocates nothing (no hipMalloc, hipFree or allocating library call).
+ * MOE_EINVAL when moe_ffn_workspace_bytes(n_hits, d, f) exceeds that size (d = 4096
+ * allows f up to about 40k), besides the argument errors of moe_expert_ffn_hits. Every
+ * call on a device shares that device's array: calls that overlap on one device (two
+ * streams, two threads) race and must be ordered by the caller.
+ */
+size_t moe_ffn_noalloc_max_bytes(void);
+int moe_expert_ffn_hits_noalloc(const float *x, const void *slot_pool, int n_slots, const int32_t *hit_slots,
+                                const float *hit_w, int n_hits, int d, int f, float *y, void *stream);
+
+/*
  * Several decode tokens at once (a small batch), every selected expert resident:
  *   y[t] = sum_j w[t][j] * FFN(slab at slot_pool + slots[t][j]*moe_slab_bytes(d,f), x[t])
  * for t < T. Each slab is read from HBM once for all the tokens that selected it (the

@@ -23,7 +23,7 @@ _lib = _abi.load()
 __all__ = [
     "MoeError", "lib", "slab_bytes", "router_topk", "Cache", "ffn_workspace_bytes", "expert_ffn_hits",
     "combine", "PinnedBuffer", "HostPool", "Runtime", "prefill_workspace_bytes", "prefill_forward", "read_stream",
-    "ffn_tokens_workspace_bytes", "expert_ffn_tokens",
+    "ffn_tokens_workspace_bytes", "expert_ffn_tokens", "ffn_noalloc_max_bytes", "expert_ffn_hits_noalloc",
 ]
 
 
@@ -173,6 +173,19 @@ def expert_ffn_hits(x, slot_pool, n_slots, hit_slots, hit_w, d, f, y, workspace,
     _check("moe_expert_ffn_hits", _lib.moe_expert_ffn_hits(
         _ptr(x), _ptr(slot_pool), n_slots, _ptr(hit_slots), _ptr(hit_w), n_hits, d, f, _ptr(y),
         _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream)))
+    return y
+
+
+def ffn_noalloc_max_bytes() -> int:
+    return int(_lib.moe_ffn_noalloc_max_bytes())
+
+
+def expert_ffn_hits_noalloc(x, slot_pool, n_slots, hit_slots, hit_w, d, f, y, stream=None):
+    """expert_ffn_hits with the library's static device scratch instead of a workspace
+    (allocates nothing; calls that overlap on one device race)."""
+    n_hits = int(hit_slots.numel())
+    _check("moe_expert_ffn_hits_noalloc", _lib.moe_expert_ffn_hits_noalloc(
+        _ptr(x), _ptr(slot_pool), n_slots, _ptr(hit_slots), _ptr(hit_w), n_hits, d, f, _ptr(y), _stream(stream)))
     return y
 
 

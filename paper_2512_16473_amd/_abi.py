@@ -66,6 +66,9 @@ SIGNATURES = [
     ("moe_ffn_workspace_bytes", c_size_t, [c_int, c_int, c_int]),
     ("moe_expert_ffn_hits", c_int, [c_void_p, c_void_p, c_int, c_void_p, c_void_p, c_int, c_int, c_int,
                                     c_void_p, c_void_p, c_size_t, c_void_p]),
+    ("moe_ffn_noalloc_max_bytes", c_size_t, []),
+    ("moe_expert_ffn_hits_noalloc", c_int, [c_void_p, c_void_p, c_int, c_void_p, c_void_p, c_int, c_int, c_int,
+                                            c_void_p, c_void_p]),
     ("moe_combine", c_int, [c_void_p, c_void_p, c_void_p, c_int, c_void_p, c_void_p]),
     ("moe_ffn_tokens_workspace_bytes", c_size_t, [c_int, c_int, c_int, c_int]),
     ("moe_expert_ffn_tokens", c_int, [c_void_p, c_void_p, c_int, c_void_p, c_void_p, c_int, c_int, c_int, c_int,

@@ -120,6 +120,24 @@ int moe_expert_ffn_hits(const float *x, const void *slot_pool, int n_slots, cons
     MOE_GUARD_END
 }
 
+size_t moe_ffn_noalloc_max_bytes(void) { return moe::kNoAllocScratchBytes; }
+
+int moe_expert_ffn_hits_noalloc(const float *x, const void *slot_pool, int n_slots, const int32_t *hit_slots,
+                                const float *hit_w, int n_hits, int d, int f, float *y, void *stream)
+{
+    MOE_GUARD_BEGIN
+    int rc = check_ffn_hits("moe_expert_ffn_hits_noalloc", x, slot_pool, n_slots, hit_slots, hit_w, n_hits, d, f, y);
+    if (rc != MOE_OK) return rc;
+    const size_t need = moe::ffn_workspace_bytes(n_hits, d, f);
+    MOE_REQUIRE(need <= moe::kNoAllocScratchBytes,
+                "moe_expert_ffn_hits_noalloc: d=%d f=%d need %zu bytes of scratch, more than its %zu", d, f, need,
+                moe::kNoAllocScratchBytes);
+    void *scratch = nullptr;
+    MOE_HIP(moe::noalloc_scratch(&scratch));
+    return run_ffn_hits(x, slot_pool, n_slots, hit_slots, hit_w, n_hits, d, f, y, scratch, stream);
+    MOE_GUARD_END
+}
+
 int moe_combine(const float *y_gpu, const float *y_host, const float *y_shared, int d, float *out, void *stream)
 {
     MOE_GUARD_BEGIN

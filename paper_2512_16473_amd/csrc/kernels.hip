@@ -16,6 +16,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "moe.h"
 #include "moe_internal.h"
 #include "stream_ops.h"
@@ -475,6 +477,34 @@ hipError_t launch_router_cpr(const float *x, const float *wr, int T, int d, int 
 }
 
 }  // namespace
+
+// Device scratch of the allocation-free hit FFN (moe_expert_ffn_hits_noalloc): the
+// job-table header, h and the split-K partials of one call live here instead of in a
+// caller workspace. One copy per device, held until the process ends; every call on a
+// device shares it, so calls that overlap on one device race. Nothing in it needs to
+// start at zero: the gate/up kernel writes the header and every h row it owns, the down
+// kernel every partial the reduce reads.
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+
+hipError_t noalloc_scratch(void **ptr)
+{
+    // Host code may not pass `scratch` itself to a kernel (its host-side name is not a
+    // device address): its address on the current device is looked up once per device.
+    static std::mutex mu;
+    static void *addr[kMaxDevices] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(mu);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        if ((e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) != hipSuccess) return e;
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
+}
 
 int device_cu_count()
 {

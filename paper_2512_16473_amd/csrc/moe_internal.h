@@ -40,6 +40,12 @@ struct FfnParams {
 size_t ffn_workspace_bytes(int max_jobs, int d, int f_max);
 void ffn_bind_workspace(FfnParams &p, void *ws, int max_jobs, int d, int f_max);
 
+// The allocation-free hit FFN's device scratch (a static device array of this many
+// bytes, one per device): noalloc_scratch returns its address on the current device.
+constexpr size_t kNoAllocScratchBytes = (size_t)8 << 20;
+constexpr int kMaxDevices = 64;
+hipError_t noalloc_scratch(void **ptr);
+
 // Events attached to the two weight-streaming kernel launches (null = no timing).
 // They are recorded by the launch itself (start and stop of that dispatch), so their
 // difference is the kernel's execution time without the dispatch gap.

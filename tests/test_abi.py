@@ -69,6 +69,16 @@ def test_argument_errors_do_not_touch_the_device():
         _abi.MOE_EINVAL                                                    # null pointers
     assert lib.moe_ffn_tokens_workspace_bytes(0, 2, 256, 512) == 0
     assert lib.moe_ffn_tokens_workspace_bytes(2, 2, 256, 512) >= 4 * 512 * 4 + 4 * 256 * 4
+    # allocation-free hit FFN: the scratch limit and the arguments checked before any HIP call
+    assert lib.moe_ffn_noalloc_max_bytes() == 8 << 20
+    a = ctypes.c_void_p(1 << 20)       # an aligned stand-in address: never dereferenced here
+    assert lib.moe_expert_ffn_hits_noalloc(a, a, 4, a, a, 2, 8192, 65536, a, None) == _abi.MOE_EINVAL
+    assert b"scratch" in lib.moe_last_error()
+    assert moe.ffn_workspace_bytes(2, 8192, 65536) > lib.moe_ffn_noalloc_max_bytes()
+    assert moe.ffn_workspace_bytes(2, 4096, 14336) <= lib.moe_ffn_noalloc_max_bytes()
+    assert lib.moe_expert_ffn_hits_noalloc(None, a, 4, a, a, 2, 64, 64, a, None) == _abi.MOE_EINVAL
+    assert lib.moe_expert_ffn_hits_noalloc(a, a, 4, a, a, 17, 64, 64, a, None) == _abi.MOE_EINVAL
+    assert lib.moe_expert_ffn_hits_noalloc(a, a, 4, a, a, 2, 60, 64, a, None) == _abi.MOE_EINVAL
     # read-stream yardstick: size, grid and pointers checked before any HIP call
     assert lib.moe_read_stream(None, 24, None, 0, None) == _abi.MOE_EINVAL
     assert b"multiple of 16" in lib.moe_last_error()
