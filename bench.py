@@ -428,6 +428,81 @@ def _kernel_record(name):
     return rec
 
 
+def geometry_sweep(args, torch, moe, synth, wl):
+    """Cache geometry x host threads (Section III-B sizing, Section IV-C trade-off): for
+    memory budgets (the paper's 24 GB card less 5 GB of non-expert weights, and the
+    58-slot "(29,2)" configuration it discusses) and for full coverage at several ways,
+    the decode loop runs with 1..16 host threads, every miss post-fetched, cold cache.
+    Each point: a fresh cache and runtime over the same host experts and inputs."""
+    import numpy as np
+    d, f, n, k, L = wl.d, wl.f, wl.n, wl.k, wl.L
+    steps_total = args.warmup + args.steps
+    world = build_world(torch, moe, synth, wl, steps_total, args.seed, 1, args.pinned_gb)
+    world["rt"].close()
+    stride, xd = world["stride"], world["xd"]
+    H = world["H"]
+    host_addrs = [world["hosts"][l % H].ptr + e * stride for l in range(L) for e in range(n)]
+    E = 3 * d * f * 2
+    if wl.name == "mixtral":
+        geoms = [(19.0, 2), (19.0, 4), (58 * E / 1e9, 2), (None, 2), (None, 4), (None, 6)]
+    else:
+        geoms = [(19.0, 4), (19.0, 6), (19.0, 8), (None, 4), (None, 6), (None, 8)]
+    threads = [int(t) for t in args.sweep_threads.split(",")]
+    streams = (torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream())
+    out = torch.empty((2, L, d), dtype=torch.float32, device="cuda")
+    hit = np.empty((L, k), np.uint8)
+    rows = []
+    for budget, M in geoms:
+        if budget is None:
+            covered, slots = L, L * M
+        else:
+            slots, covered = moe.cache_geometry(int(budget * 1e9), E, M, L)
+        pool = torch.zeros(max(1, covered * M) * stride, dtype=torch.uint8, device="cuda") if covered else None
+        for t in threads:
+            cache = moe.Cache(covered, n, M, k)
+            hp = moe.HostPool(t)
+            rt = moe.Runtime(d, f, n, k, M, L, world["wr"], pool, host_addrs, cache, hp)
+            for s in range(args.warmup):
+                rt.decode_step(xd[s], out[s % 2], streams)
+            torch.cuda.synchronize()
+            rt.sync()
+            rt.reset_stats()
+            anyh = allh = 0
+            t0 = time.perf_counter()
+            for s in range(args.warmup, steps_total):
+                rt.decode_step(xd[s], out[s % 2], streams, hit=hit)
+                anyh += int(hit.any(axis=1).sum())
+                allh += int(hit.all(axis=1).sum())
+            torch.cuda.synchronize()
+            rt.sync()
+            dt = time.perf_counter() - t0
+            st = rt.stats()
+            K = args.steps
+            sel = st["expert_hits"] + st["expert_misses"]
+            row = {"budget_gb": None if budget is None else round(budget, 2), "ways": M, "slots": slots,
+                   "covered_layers": covered, "host_threads": t, "tokens_per_s": round(K / dt, 2),
+                   "expert_hit_rate": round(st["expert_hits"] / max(1, sel), 4),
+                   "any_hit": round(anyh / (K * L), 4), "all_hit": round(allh / (K * L), 4),
+                   "misses_per_token": round(st["expert_misses"] / K, 2),
+                   "host_ffn_ms_per_token": round(st["host_ffn_ms"] / K, 2),
+                   "fills_per_token": round(st["fills"] / K, 2)}
+            log(json.dumps(row))
+            rows.append(row)
+            rt.close()
+            cache.close()
+            hp.close()
+        del pool
+        torch.cuda.empty_cache()
+    return {
+        "metric": "decode MoE-stage tokens/s by cache geometry and host threads",
+        "value": None, "unit": "tokens/s", "n_gpus": 1, "higher_is_better": True, "data": "synthetic",
+        "config": {"workload": wl.desc, "expert_bytes": E, "warmup": args.warmup, "steps": args.steps,
+                   "post_fetch": "every miss (Section III-A step 3); parity (waits)", "cache_start": "cold",
+                   "host_expert_layers_distinct": H},
+        "rows": rows,
+    }
+
+
 def measured_traffic(args, kernel, bytes_per_launch):
     """HBM bytes per launch of `kernel` (k_gate_up, k_down) for this run: the ratio of
     counted (rocprofv3 FETCH_SIZE/WRITE_SIZE, scaled by the copy calibration) to
@@ -658,6 +733,9 @@ def main():
     ap.add_argument("--pcie", action="store_true", help="only measure host-to-device expert copies")
     ap.add_argument("--small-batch", action="store_true",
                     help="only time multi-token decode (T = 1..64) with every expert resident")
+    ap.add_argument("--sweep", action="store_true",
+                    help="only run the cache-geometry x host-threads sweep (mixtral or phi)")
+    ap.add_argument("--sweep-threads", default="1,2,4,8,16", help="host thread counts of --sweep")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB 5 times (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -691,6 +769,9 @@ def main():
         return
     if args.hit_study:
         print(json.dumps(hit_study(args, torch, moe, synth, wl)), flush=True)
+        return
+    if args.sweep:
+        print(json.dumps(geometry_sweep(args, torch, moe, synth, wl)), flush=True)
         return
     if wl.prefill:
         print(json.dumps(bench_prefill(args, torch, moe, synth, wl)), flush=True)

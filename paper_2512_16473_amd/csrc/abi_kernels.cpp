@@ -96,7 +96,7 @@ int run_ffn_hits(const float *x, const void *slot_pool, int n_slots, const int32
     p.f = f;
     moe::ffn_bind_workspace(p, workspace, n_hits, d, f);
     hipStream_t s = (hipStream_t)stream;
-    MOE_HIP(moe::launch_ffn_stream(p, s, nullptr, nullptr));
+    MOE_HIP(moe::launch_ffn_stream(p, s, nullptr));
     MOE_HIP(moe::launch_ffn_reduce(p, nullptr, y, s));
     return MOE_OK;
 }

@@ -172,6 +172,22 @@ __global__ __launch_bounds__(kBlock) void k_gate_up(FfnParams p)
     }
 }
 
+// True in the one work group of the grid that arrives last at this point. Every work
+// group calls it once, with all its threads; the partial results each wrote before the
+// call are visible to the last one after it returns (device-scope fences around the
+// arrival counter, which the caller zeroed before the launch or the last group resets).
+__device__ __forceinline__ bool arrive_last(unsigned *ticket)
+{
+    __shared__ int last;
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) last = atomicAdd(ticket, 1u) == gridDim.x - 1;
+    __syncthreads();
+    if (!last) return false;
+    __threadfence();
+    return true;
+}
+
 // ---------------------------------------------------------------------------
 // Down: partial[part0[j] + s][i] = w_j * sum over segment s of W2_j[i, c] h_j[c].
 // The (segment, row) pairs of all active jobs, in (job, segment, row) order, are
@@ -287,6 +303,72 @@ __global__ __launch_bounds__(kBlock) void k_combine(const float *a, const float 
 }
 
 // ---------------------------------------------------------------------------
+// Top-k of n fp64 logits held in LDS, by one wave: the k largest (ties to the lower
+// id; NaN ranked as -inf so ids are always valid), ordered (logit desc, id asc), with
+// weights w_r = exp(l_r - l_0) / sum_{s<k} exp(l_s - l_0), the softmax restricted to
+// the selected set (equal to p_S / sum p_S). Lanes r < k write idx[r], w[r] (and the
+// mailbox entries when mbox is set).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void select_topk(const double *logit, int n, int k, int lane, int32_t *idx, float *wout,
+                                            RouteMailbox *mbox)
+{
+    constexpr int kPer = MOE_MAX_EXPERTS / kWave;
+    double v[kPer];
+    bool taken[kPer];
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        const int e = q * kWave + lane;
+        double l = (e < n) ? logit[e] : -INFINITY;
+        if (l != l) l = -INFINITY;
+        v[q] = l;
+        taken[q] = (e >= n);
+    }
+    // Lane r keeps the r-th selected (logit, id).
+    double my_l = -INFINITY;
+    int my_i = -1;
+    for (int r = 0; r < k; ++r) {
+        double bv = -INFINITY;
+        int bi = 0x7fffffff;
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            const int e = q * kWave + lane;
+            if (!taken[q] && (v[q] > bv || (v[q] == bv && e < bi))) {
+                bv = v[q];
+                bi = e;
+            }
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+            const double ov = __shfl_xor(bv, o, kWave);
+            const int oi = __shfl_xor(bi, o, kWave);
+            if (ov > bv || (ov == bv && oi < bi)) {
+                bv = ov;
+                bi = oi;
+            }
+        }
+        if (lane == r) {
+            my_l = bv;
+            my_i = bi;
+        }
+#pragma unroll
+        for (int q = 0; q < kPer; ++q)
+            if (q * kWave + lane == bi) taken[q] = true;
+    }
+    const double l0 = __shfl(my_l, 0, kWave);
+    const double ex = (lane < k) ? exp(my_l - l0) : 0.0;
+    const double z = wave_sum(ex);
+    if (lane < k) {
+        const float wr32 = (float)(ex / z);
+        idx[lane] = my_i;
+        wout[lane] = wr32;
+        if (mbox) {
+            mbox->idx[lane] = my_i;
+            mbox->w[lane] = wr32;
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
 // Router: one block per token. x is staged in LDS; each wave takes whole experts,
 // issuing all CPR 16-byte loads of a router row at once, and accumulates the exact
 // fp64 products of the fp32 inputs. Wave 0 then selects the top-k in fp64 (ties to
@@ -322,10 +404,8 @@ __global__ __launch_bounds__(kRouterBlock) void k_router(const float *X, const f
         for (int mb = 0; mb < CPR; mb += kStep) {
             float4 wvv[kStep];
 #pragma unroll
-            for (int m = 0; m < kStep; ++m) {
-                const int q = (mb + m) * kWave + lane;
-                wvv[m] = q < nq ? w4[q] : make_float4(0, 0, 0, 0);
-            }
+            for (int m = 0; m < kStep; ++m)   // unconditional (xs is zero past the row)
+                wvv[m] = w4[min((mb + m) * kWave + lane, nq - 1)];
 #pragma unroll
             for (int m = 0; m < kStep; ++m) {
                 const float4 xv = xs[(mb + m) * kWave + lane];
@@ -340,66 +420,168 @@ __global__ __launch_bounds__(kRouterBlock) void k_router(const float *X, const f
     }
     __syncthreads();
     if (wv == 0) {
-        constexpr int kPer = MOE_MAX_EXPERTS / kWave;
-        double v[kPer];
-        bool taken[kPer];
-#pragma unroll
-        for (int q = 0; q < kPer; ++q) {
-            const int e = q * kWave + lane;
-            double l = (e < n) ? logit[e] : -INFINITY;
-            if (l != l) l = -INFINITY;
-            v[q] = l;
-            taken[q] = (e >= n);
-        }
-        // Lane r keeps the r-th selected (logit, id): order is logit desc, id asc.
-        double my_l = -INFINITY;
-        int my_i = -1;
-        for (int r = 0; r < k; ++r) {
-            double bv = -INFINITY;
-            int bi = 0x7fffffff;
-#pragma unroll
-            for (int q = 0; q < kPer; ++q) {
-                const int e = q * kWave + lane;
-                if (!taken[q] && (v[q] > bv || (v[q] == bv && e < bi))) {
-                    bv = v[q];
-                    bi = e;
-                }
-            }
-#pragma unroll
-            for (int o = 32; o > 0; o >>= 1) {
-                const double ov = __shfl_xor(bv, o, kWave);
-                const int oi = __shfl_xor(bi, o, kWave);
-                if (ov > bv || (ov == bv && oi < bi)) {
-                    bv = ov;
-                    bi = oi;
-                }
-            }
-            if (lane == r) {
-                my_l = bv;
-                my_i = bi;
-            }
-#pragma unroll
-            for (int q = 0; q < kPer; ++q)
-                if (q * kWave + lane == bi) taken[q] = true;
-        }
-        // w_r = exp(l_r - l_0) / sum_{s<k} exp(l_s - l_0), the softmax restricted to
-        // the selected set (equal to p_S / sum p_S).
-        const double l0 = __shfl(my_l, 0, kWave);
-        const double ex = (lane < k) ? exp(my_l - l0) : 0.0;
-        const double z = wave_sum(ex);
-        if (lane < k) {
-            const float wr32 = (float)(ex / z);
-            idx[(size_t)t * k + lane] = my_i;
-            wout[(size_t)t * k + lane] = wr32;
-            if (mbox) {
-                mbox->idx[lane] = my_i;
-                mbox->w[lane] = wr32;
-            }
-        }
+        select_topk(logit, n, k, lane, idx + (size_t)t * k, wout + (size_t)t * k, mbox);
     } else if (x_host) {
         // The other waves hand the hidden state to the host for the miss path.
         float4 *xh = reinterpret_cast<float4 *>(x_host);
         for (int q = threadIdx.x - kWave; q < nq; q += kRouterBlock - kWave) xh[q] = xs[q];
+    }
+    if (mbox) {
+        __threadfence_system();
+        __syncthreads();
+        if (threadIdx.x == 0) __hip_atomic_store(&mbox->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Single-token decode router over many work groups. Item (e, s) = expert e, segment s
+// (kRouteSeg floats) of its router row; wave `item` of the grid streams that segment
+// (four 16-byte loads per lane, all in flight at once) against the same slice of x and
+// stores the fp64 partial logit part[e * nseg + s]. The work group that arrives last
+// sums each expert's segments in order, selects the top-k, hands the routing and x to
+// the host (mailbox, then the sequence number with a system-scope release) and resets
+// the arrival counter. Work group 0 installs the layer's mirror row at its start.
+// ---------------------------------------------------------------------------
+constexpr int kRouteSeg = 1024;
+
+__global__ __launch_bounds__(kBlock) void k_route1(const float *x, const float *Wr, int d, int n, int k,
+                                                   int32_t *idx, float *wout, double *part, unsigned *ticket,
+                                                   RouteMailbox *mbox, float *x_host, int32_t seq,
+                                                   const int32_t *row_src, int32_t *row_dst)
+{
+    if (blockIdx.x == 0 && row_src)
+        for (int i = threadIdx.x; i < n; i += kBlock) row_dst[i] = row_src[i];
+    constexpr int kPerLane = kRouteSeg / (4 * kWave);   // float4 loads per lane
+    const int lane = threadIdx.x & (kWave - 1);
+    const int item = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
+    const int nseg = (d + kRouteSeg - 1) / kRouteSeg;
+    const int nq = d >> 2;
+    if (item < n * nseg) {
+        const int e = item / nseg;
+        const int q0 = (item - e * nseg) * (kRouteSeg / 4);
+        const float4 *w4 = reinterpret_cast<const float4 *>(Wr + (size_t)e * d);
+        const float4 *x4 = reinterpret_cast<const float4 *>(x);
+        float4 wv[kPerLane], xv[kPerLane];
+#pragma unroll
+        for (int m = 0; m < kPerLane; ++m) {   // unconditional loads; past the row: zeroed x
+            const int q = min(q0 + m * kWave + lane, nq - 1);
+            wv[m] = w4[q];
+            xv[m] = x4[q];
+        }
+#pragma unroll
+        for (int m = 0; m < kPerLane; ++m)
+            if (q0 + m * kWave + lane >= nq) xv[m] = make_float4(0, 0, 0, 0);
+        double acc = 0.0;
+#pragma unroll
+        for (int m = 0; m < kPerLane; ++m) {
+            acc += (double)wv[m].x * (double)xv[m].x;
+            acc += (double)wv[m].y * (double)xv[m].y;
+            acc += (double)wv[m].z * (double)xv[m].z;
+            acc += (double)wv[m].w * (double)xv[m].w;
+        }
+        acc = wave_sum(acc);
+        if (lane == 0) part[item] = acc;
+    }
+    if (!arrive_last(ticket)) return;
+    __shared__ double logit[MOE_MAX_EXPERTS];
+    for (int e = threadIdx.x; e < n; e += kBlock) {
+        double l = 0.0;
+        for (int sg = 0; sg < nseg; ++sg) l += part[e * nseg + sg];
+        logit[e] = l;
+    }
+    if (threadIdx.x == 0) *ticket = 0u;
+    __syncthreads();
+    const int wv0 = threadIdx.x >> 6;
+    if (wv0 == 0) {
+        select_topk(logit, n, k, lane, idx, wout, mbox);
+    } else if (x_host) {
+        const float4 *x4 = reinterpret_cast<const float4 *>(x);
+        float4 *xh = reinterpret_cast<float4 *>(x_host);
+        for (int q = threadIdx.x - kWave; q < nq; q += kBlock - kWave) xh[q] = x4[q];
+    }
+    if (mbox) {
+        __threadfence_system();
+        __syncthreads();
+        if (threadIdx.x == 0) __hip_atomic_store(&mbox->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Single-token decode router in one work group of 512 threads, for router matrices of
+// at most kRouteBlkItems (expert, segment) items whose segment count divides 8: wave w
+// takes items w, w + 8, ... (at most eight, all loads issued at once), which all lie in
+// segment w mod nseg, so the wave loads that slice of x once. The fp64 partial logits go
+// to LDS and wave 0 sums each expert's segments in order and selects the top-k. One work
+// group needs no arrival counter or device-scope fence; the mailbox hand-off is that of
+// k_router.
+// ---------------------------------------------------------------------------
+constexpr int kRouteBlkThreads = 512;
+constexpr int kRouteBlkWaves = kRouteBlkThreads / kWave;
+constexpr int kRouteBlkPerWave = 8;
+constexpr int kRouteBlkItems = kRouteBlkWaves * kRouteBlkPerWave;
+
+__global__ __launch_bounds__(kRouteBlkThreads) void k_router_blk(const float *x, const float *Wr, int d, int n, int k,
+                                                                 int32_t *idx, float *wout, RouteMailbox *mbox,
+                                                                 float *x_host, int32_t seq, const int32_t *row_src,
+                                                                 int32_t *row_dst)
+{
+    if (row_src)
+        for (int i = threadIdx.x; i < n; i += kRouteBlkThreads) row_dst[i] = row_src[i];
+    constexpr int kPerLane = kRouteSeg / (4 * kWave);
+    __shared__ double part[kRouteBlkItems];
+    __shared__ double logit[MOE_MAX_EXPERTS];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wv = threadIdx.x >> 6;
+    const int nseg = (d + kRouteSeg - 1) / kRouteSeg;   // divides kRouteBlkWaves
+    const int items = n * nseg;
+    const int nq = d >> 2;
+    const int q0 = (wv % nseg) * (kRouteSeg / 4);        // this wave's slice of every row
+    const float4 *x4 = reinterpret_cast<const float4 *>(x);
+    float4 xq[kPerLane], wq[kRouteBlkPerWave][kPerLane];
+    // Every load is unconditional (a branch per load would make each one wait for the
+    // previous): positions past the row read its last chunk, items past the end the
+    // last row, and those values are zeroed after the loads.
+#pragma unroll
+    for (int m = 0; m < kPerLane; ++m) xq[m] = x4[min(q0 + m * kWave + lane, nq - 1)];
+#pragma unroll
+    for (int u = 0; u < kRouteBlkPerWave; ++u) {
+        const int item = wv + u * kRouteBlkWaves;
+        const float4 *w4 = reinterpret_cast<const float4 *>(Wr + (size_t)min(item / nseg, n - 1) * d);
+#pragma unroll
+        for (int m = 0; m < kPerLane; ++m) wq[u][m] = w4[min(q0 + m * kWave + lane, nq - 1)];
+    }
+#pragma unroll
+    for (int m = 0; m < kPerLane; ++m)
+        if (q0 + m * kWave + lane >= nq) xq[m] = make_float4(0, 0, 0, 0);
+#pragma unroll
+    for (int u = 0; u < kRouteBlkPerWave; ++u) {
+        // one item at a time: keeps the scheduler from widening every loaded value to
+        // fp64 at once (which would not fit the registers)
+        __builtin_amdgcn_sched_barrier(0);
+        double acc = 0.0;
+#pragma unroll
+        for (int m = 0; m < kPerLane; ++m) {
+            acc += (double)wq[u][m].x * (double)xq[m].x;
+            acc += (double)wq[u][m].y * (double)xq[m].y;
+            acc += (double)wq[u][m].z * (double)xq[m].z;
+            acc += (double)wq[u][m].w * (double)xq[m].w;
+        }
+        acc = wave_sum(acc);
+        const int item = wv + u * kRouteBlkWaves;
+        if (lane == 0 && item < items) part[item] = acc;
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < n; e += kRouteBlkThreads) {
+        double l = 0.0;
+        for (int sg = 0; sg < nseg; ++sg) l += part[e * nseg + sg];
+        logit[e] = l;
+    }
+    __syncthreads();
+    if (wv == 0) {
+        select_topk(logit, n, k, lane, idx, wout, mbox);
+    } else if (x_host) {
+        float4 *xh = reinterpret_cast<float4 *>(x_host);
+        for (int q = threadIdx.x - kWave; q < nq; q += kRouteBlkThreads - kWave) xh[q] = x4[q];
     }
     if (mbox) {
         __threadfence_system();
@@ -559,7 +741,35 @@ hipError_t launch_router(const float *x, const float *wr, int T, int d, int n, i
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_ffn_stream(const FfnParams &p, hipStream_t s, const FfnEvents *ev, hipEvent_t after_down)
+size_t route1_scratch_bytes(int n, int d)
+{
+    const size_t nseg = (size_t)((d + kRouteSeg - 1) / kRouteSeg);
+    return align256(sizeof(double) * (size_t)n * nseg) + 256;   // partial logits, then the counter
+}
+
+hipError_t launch_route1(const float *x, const float *wr, int d, int n, int k, int32_t *idx, float *w,
+                         void *scratch, hipStream_t s, RouteMailbox *mbox, float *x_host, int32_t seq,
+                         const int32_t *row_src, int32_t *row_dst)
+{
+    const int nseg = (d + kRouteSeg - 1) / kRouteSeg;
+    if (!row_dst) row_src = nullptr;
+    if (n * nseg <= kRouteBlkItems && kRouteBlkWaves % nseg == 0) {   // one work group reads it all at once
+        clear_launch_error();
+        hipLaunchKernelGGL(k_router_blk, dim3(1), dim3(kRouteBlkThreads), 0, s, x, wr, d, n, k, idx, w, mbox, x_host,
+                           seq, row_src, row_dst);
+        return hipGetLastError();
+    }
+    const int blocks = (n * nseg + kWavesPerBlock - 1) / kWavesPerBlock;
+    double *part = static_cast<double *>(scratch);
+    unsigned *ticket = reinterpret_cast<unsigned *>(static_cast<uint8_t *>(scratch) +
+                                                    align256(sizeof(double) * (size_t)n * nseg));
+    clear_launch_error();
+    hipLaunchKernelGGL(k_route1, dim3(blocks), dim3(kBlock), 0, s, x, wr, d, n, k, idx, w, part, ticket, mbox,
+                       x_host, seq, row_src, row_dst);
+    return hipGetLastError();
+}
+
+hipError_t launch_ffn_stream(const FfnParams &p, hipStream_t s, const FfnEvents *ev)
 {
     // Upper bound of the gate/up rows (every routed job active); waves with no row exit.
     const int rows_max = p.k * p.f + (p.shared ? p.f_shared : 0);
@@ -573,9 +783,7 @@ hipError_t launch_ffn_stream(const FfnParams &p, hipStream_t s, const FfnEvents 
         hipExtLaunchKernelGGL(k_down, dim3(blocks), dim3(kBlock), 0, s, ev->dn_start, ev->dn_stop, 0, p);
     else
         hipLaunchKernelGGL(k_down, dim3(blocks), dim3(kBlock), 0, s, p);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (after_down && (e = hipEventRecord(after_down, s)) != hipSuccess) return e;
-    return hipSuccess;
+    return hipGetLastError();
 }
 
 hipError_t launch_ffn_reduce(const FfnParams &p, const float *y_extra, float *out, hipStream_t s)

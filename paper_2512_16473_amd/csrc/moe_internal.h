@@ -63,6 +63,18 @@ struct RouteMailbox {
     float w[MOE_MAX_TOPK_INTERNAL];
 };
 
+// Single-token decode router, one wave per (expert, 1024-float segment of its router
+// row). Up to 64 such items: one work group of 1024 threads; more: one wave per item
+// over many work groups, the last work group to finish (an arrival counter, which it
+// resets) summing the segments in order. Either way the top-k is selected and the
+// routing and x are handed to the host through the mailbox. scratch: device, >=
+// route1_scratch_bytes(n, d), zero before the first call. row_src/row_dst as for
+// launch_router.
+size_t route1_scratch_bytes(int n, int d);
+hipError_t launch_route1(const float *x, const float *wr, int d, int n, int k, int32_t *idx, float *w,
+                         void *scratch, hipStream_t s, RouteMailbox *mbox, float *x_host, int32_t seq,
+                         const int32_t *row_src, int32_t *row_dst);
+
 // mbox/x_host (device addresses of host memory, nullable) are only used when T == 1.
 // row_src (device address of host memory, nullable; T == 1 only): n int32 copied to
 // row_dst by the kernel before it exits, i.e. before any later kernel on the stream.
@@ -70,9 +82,8 @@ hipError_t launch_router(const float *x, const float *wr, int T, int d, int n, i
                          int32_t *idx, float *w, hipStream_t s, RouteMailbox *mbox = nullptr,
                          float *x_host = nullptr, int32_t seq = 0, const int32_t *row_src = nullptr,
                          int32_t *row_dst = nullptr);
-// gate/up/SiLU then down; `after_down` (nullable) is recorded right after the down kernel.
-hipError_t launch_ffn_stream(const FfnParams &p, hipStream_t s, const FfnEvents *ev,
-                             hipEvent_t after_down);
+// gate/up/SiLU then down (split-K partials for the reduce).
+hipError_t launch_ffn_stream(const FfnParams &p, hipStream_t s, const FfnEvents *ev);
 // out = sum over active jobs of weight * sum of split partials (+ y_extra).
 hipError_t launch_ffn_reduce(const FfnParams &p, const float *y_extra, float *out, hipStream_t s);
 hipError_t launch_combine(const float *a, const float *b, const float *c, int d, float *out,

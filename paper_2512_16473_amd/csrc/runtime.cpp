@@ -61,6 +61,7 @@ struct moe_runtime {
     float *d_w = nullptr;           // [k]
     void *d_ws = nullptr;
     size_t ws_bytes = 0;
+    void *d_route = nullptr;        // decode router: partial logits + arrival counter (zeroed once)
 
     // coherent pinned host memory shared with the kernels (host address, device address)
     moe::RouteMailbox *mbox = nullptr, *mbox_dev = nullptr;
@@ -112,6 +113,7 @@ void release(moe_runtime *rt)
     if (rt->d_idx) (void)hipFree(rt->d_idx);
     if (rt->d_w) (void)hipFree(rt->d_w);
     if (rt->d_ws) (void)hipFree(rt->d_ws);
+    if (rt->d_route) (void)hipFree(rt->d_route);
     if (rt->mbox) (void)hipHostFree(rt->mbox);
     if (rt->h_x) (void)hipHostFree(rt->h_x);
     if (rt->h_y) (void)hipHostFree(rt->h_y);
@@ -222,6 +224,9 @@ int moe_runtime_create(const moe_layer_desc *desc, moe_runtime **out)
     const int fmax = D.f > D.f_shared ? D.f : D.f_shared;
     rt->ws_bytes = moe::ffn_workspace_bytes(D.k + 1, D.d, fmax);
     if ((e = hipMalloc(&rt->d_ws, rt->ws_bytes)) != hipSuccess) return fail(e, "hipMalloc(workspace)");
+    const size_t route_bytes = moe::route1_scratch_bytes(D.n, D.d);
+    if ((e = hipMalloc(&rt->d_route, route_bytes)) != hipSuccess) return fail(e, "hipMalloc(router scratch)");
+    if ((e = hipMemset(rt->d_route, 0, route_bytes)) != hipSuccess) return fail(e, "hipMemset(router scratch)");
     if ((e = hipMalloc((void **)&rt->d_slotmap, sizeof(int32_t) * nh)) != hipSuccess) return fail(e, "hipMalloc");
     if ((e = hipMalloc((void **)&rt->d_idx, sizeof(int32_t) * D.k)) != hipSuccess) return fail(e, "hipMalloc");
     if ((e = hipMalloc((void **)&rt->d_w, sizeof(float) * D.k)) != hipSuccess) return fail(e, "hipMalloc");
@@ -322,8 +327,8 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
     // installs the mirror row before the hit kernels read it.
     const int32_t seq = ++rt->seq;
     const float *wr = D.w_router + (size_t)layer * n * d;
-    MOE_HIP(moe::launch_router(x_dev, wr, 1, d, n, k, rt->d_idx, rt->d_w, sc, rt->mbox_dev, rt->h_x_dev, seq,
-                               install ? rt->h_rows_dev + (size_t)layer * n : nullptr,
+    MOE_HIP(moe::launch_route1(x_dev, wr, d, n, k, rt->d_idx, rt->d_w, rt->d_route, sc, rt->mbox_dev, rt->h_x_dev,
+                               seq, install ? rt->h_rows_dev + (size_t)layer * n : nullptr,
                                rt->d_slotmap + (size_t)layer * n));
 
     // Hit experts on the device (slots from the device mirror of the table).
@@ -357,7 +362,7 @@ int moe_layer_forward(moe_runtime *rt, int layer, const float *x_dev, float *out
         ev.dn_start = rec.ev[2];
         ev.dn_stop = rec.ev[3];
     }
-    MOE_HIP(moe::launch_ffn_stream(p, sc, rt->timing ? &ev : nullptr, nullptr));
+    MOE_HIP(moe::launch_ffn_stream(p, sc, rt->timing ? &ev : nullptr));
 
     // Step 1 on the host: wait for the routing, then check + LRU update.
     const double t0 = now_ms();

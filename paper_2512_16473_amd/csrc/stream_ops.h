@@ -15,10 +15,15 @@ typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ float bf_lo(uint32_t v) { return __uint_as_float(v << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
 
-// 16-byte load marked nontemporal (streamed weights are read exactly once).
+typedef const __attribute__((address_space(1))) u32x4_t global_u32x4_t;
+
+// 16-byte load marked nontemporal (streamed weights are read exactly once), from the
+// global address space: the slab pointers come through LDS tables, and without the cast
+// the compiler emits flat loads, which also count against the LDS wait counter, so every
+// wait for an LDS read would wait for the weight loads in flight as well.
 __device__ __forceinline__ uint4 stream_load(const uint4 *p)
 {
-    const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+    const u32x4_t v = __builtin_nontemporal_load((global_u32x4_t *)(p));
     return make_uint4(v.x, v.y, v.z, v.w);
 }
 
