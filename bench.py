@@ -628,9 +628,9 @@ def bench_prefill(args, torch, moe, synth, wl):
     }
 
 
-def all_resident_and_prefill(args, torch, moe, synth, wl, world, xd, tokens=64, prompts=4):
+def all_resident_and_prefill(args, torch, moe, synth, wl, world, xd, tokens=64, prompts=4, prefill=True):
     """The GPU-bound regime on the same weights: every expert of every layer resident
-    (a static cache holding all n experts; MI355X's HBM holds a Mixtral-sized expert set),
+    (a static cache holding all n experts; MI355X's HBM holds each workload's expert set),
     so each decode token runs router + hit FFN + reduce per layer with no host work and
     no copies. Timed once with the kernel timing events off (tokens/s) and once with
     them on (kernel rooflines). Then a 512-token prompt through the same resident
@@ -643,7 +643,8 @@ def all_resident_and_prefill(args, torch, moe, synth, wl, world, xd, tokens=64, 
     pool = torch.empty(L * n * stride, dtype=torch.uint8, device="cuda")
     t0 = time.perf_counter()
     cache = moe.Cache(L, n, n, k, policy="static", static_content=content)
-    rt = moe.Runtime(d, f, n, k, n, L, world["wr"], pool, host_addrs, cache, world["hp"])   # loads every slab
+    rt = moe.Runtime(d, f, n, k, n, L, world["wr"], pool, host_addrs, cache, world["hp"], f_shared=wl.f_shared,
+                     shared_pool=world["shared"])   # loads every slab
     torch.cuda.synchronize()
     log(f"all-resident world: {pool.numel() / 1e9:.1f} GB of experts loaded in {time.perf_counter() - t0:.1f}s")
     streams = (torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream())
@@ -668,7 +669,7 @@ def all_resident_and_prefill(args, torch, moe, synth, wl, world, xd, tokens=64, 
     rt.set_timing(False)
     rt.close()
     cache.close()
-    alg_layer = k * 3 * d * f * 2 + n * d * 4
+    alg_layer = k * 3 * d * f * 2 + n * d * 4 + 3 * d * wl.f_shared * 2
     us_layer = dt / (tokens * L) * 1e6
     gu = st["gate_up_bytes"] / (st["gate_up_ms"] * 1e-3) / 1e9
     dn = st["down_bytes"] / (st["down_ms"] * 1e-3) / 1e9
@@ -687,6 +688,10 @@ def all_resident_and_prefill(args, torch, moe, synth, wl, world, xd, tokens=64, 
         "hit_ffn_us_per_layer": round((st["gate_up_ms"] + st["down_ms"]) / st["gate_up_launches"] * 1e3, 2),
     }
     log(json.dumps(res))
+    if not prefill:
+        del pool
+        torch.cuda.empty_cache()
+        return res, None
     X = torch.from_numpy(synth.iid_states(synth.seed_for(args.seed, "prefill", "prompt"), 512, d)).cuda()
     pf = prefill_pass(torch, moe, pool, world["wr"], X, d, f, n, k, L, 2, prompts)
     pf["what"] = (f"one 512-token prompt (i.i.d. N(0,1)) through the {L} resident layers; 2 warm-up + {prompts} "
@@ -717,7 +722,7 @@ def main():
     ap.add_argument("--cpu-baseline-s", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-resident", action="store_true",
-                    help="skip the all-resident decode and prefill sub-measurements of the Mixtral line")
+                    help="skip the all-resident decode sub-measurement (and the prefill one of the Mixtral line)")
     ap.add_argument("--policy", default="lru", choices=["lru", "fifo", "static"],
                     help="cache replacement policy (Section IV-D; the paper's is LRU)")
     ap.add_argument("--ways", type=int, default=0,
@@ -920,9 +925,12 @@ def main():
             "host_ffn_ms_per_token": round(s2["host_ffn_ms"] / K, 3)}
         log(json.dumps(result["bounded_post_fetch"]))
         rt = rt2
-    if args.workload == "mixtral" and not args.no_resident:
+    if not args.no_resident and wl.name != "tiny":
         rt.close()
-        result["all_resident"], result["prefill"] = all_resident_and_prefill(args, torch, moe, synth, wl, world, xd)
+        result["all_resident"], pf = all_resident_and_prefill(args, torch, moe, synth, wl, world, xd,
+                                                              prefill=wl.name == "mixtral")
+        if pf is not None:
+            result["prefill"] = pf
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, world, args.seed, args.cpu_baseline_s, args.warmup)
     else:
