@@ -19,10 +19,10 @@ class World:
     """A decode world on the GPU: router weights, slot pool, pinned host experts,
     shared experts, AR(1) hidden states, library runtime."""
 
-    def __init__(self, name, L=None, T=None, ways=None, threads=4, seed=0, policy="lru", covered=None):
+    def __init__(self, name, L=None, T=None, ways=None, threads=4, seed=0, policy="lru", covered=None, wl=None):
         torch = torch_cuda()
         import paper_2512_16473_amd as moe
-        wl = synth.WORKLOADS[name]
+        wl = wl or synth.WORKLOADS[name]
         self.wl = wl
         self.L = L or wl.L
         self.T = T or wl.T
@@ -142,6 +142,22 @@ def test_runtime_full_shapes(name, L, T, layers):
     world = World(name, L=L, T=T, threads=8)
     idx, w, hit, out = world.run(T)
     worst = _check_trace(world, idx, w, hit, out, T, layers, lambda t, l: True)
+    say("  worst max|err|/RMS", worst)
+
+
+@pytest.mark.parametrize("d,n,k,ways", [(3072, 16, 4, 8), (2048, 40, 3, 6), (8192, 8, 2, 4), (768, 256, 16, 16)])
+def test_runtime_router_shapes(d, n, k, ways):
+    """The single-token decode routers at their edges, through the whole path: a router
+    matrix read by one work group (at most 64 (expert, 1024-float segment) items, segment
+    count dividing 8: d = 8192 with 8 segments) and by many work groups with the arrival
+    counter (3 segments; 80 items; 256 experts top-16), over many layer calls so the
+    counter's reset is exercised. Routing, trace and every output against the oracle."""
+    oracle.set_threads(min(16, os.cpu_count() or 1))
+    say("runtime router shape", d, n, k, ways)
+    wl = synth.Workload("tiny", d=d, f=256, n=n, k=k, L=2, T=12, ways=ways, w_std=None)
+    world = World("tiny", wl=wl)
+    idx, w, hit, out = world.run(wl.T)
+    worst = _check_trace(world, idx, w, hit, out, wl.T, {0, 1}, lambda t, l: True)
     say("  worst max|err|/RMS", worst)
 
 
