@@ -623,8 +623,13 @@ inline void clear_launch_error() { (void)hipGetLastError(); }
 template <int CPL>
 hipError_t launch_gate_up_cpl(const FfnParams &p, int items, hipStream_t s, hipEvent_t e0, hipEvent_t e1)
 {
+    // Up to 4 x the resident work groups (more waves, each with a few row pairs, hide the
+    // load latency better than fewer longer-lived ones), fewer while that would leave
+    // under two row pairs per wave (each wave loads x before its first row).
     static int occ = 0;
-    const int cap = blocks_per_cu(k_gate_up<CPL>, kBlock, &occ) * device_cu_count() * 4;
+    const int resident = blocks_per_cu(k_gate_up<CPL>, kBlock, &occ) * device_cu_count();
+    int cap = resident * 4;
+    while (cap > resident && (int64_t)cap * kWavesPerBlock * 2 > items) cap /= 2;
     int blocks = (items + kWavesPerBlock - 1) / kWavesPerBlock;
     blocks = blocks < 1 ? 1 : (blocks > cap ? cap : blocks);
     clear_launch_error();
