@@ -15,8 +15,9 @@
 //
 // With about T k / n tokens per expert (128 for a 512-token prompt on 8 experts, top-2)
 // the GEMMs are bound by reading the expert weights from HBM, so the kernel is built to
-// keep many weight bytes in flight: the weight operand goes straight from HBM into MFMA
-// registers, several K steps ahead, and only the token tile is staged through LDS.
+// keep many weight bytes in flight: each wave loads its own weight rows into registers,
+// several K steps ahead, with whole cache lines per load instruction, and only the token
+// tile is shared through LDS.
 // Work items (expert, M tile, N tile, K split) are laid out so that every item of one
 // expert lands on the same XCD (work group b runs on XCD b mod 8), where its token rows
 // stay in that XCD's L2.
@@ -152,18 +153,15 @@ struct GemmArgs {
 };
 
 // Grouped GEMM with the weight operand fed from HBM into MFMA registers without a shared
-// staging buffer (gate/up directly, down through each wave's own LDS region; see
-// gemm_k_loop).
+// staging buffer: each wave loads its own weight rows and passes them through its own
+// LDS region into the operand layout (see gemm_k_loop).
 //
 // A work group (8 waves) owns up to 192 tokens of one expert and 128 kNB weight rows; each
 // wave owns 16 kNB of the weight rows (kNB 16-row MFMA column blocks) and all the tokens
 // (twelve 16-row blocks). In v_mfma_f32_16x16x32_bf16 the B operand of lane l is 8
 // consecutive K values of column l mod 16, the four lanes l mod 16 + 16 i covering 32
-// consecutive K values, so each lane can load its 16-byte B pieces from its own weight
-// row: each weight byte is loaded once per work group, and every load instruction reads
-// 64 contiguous bytes from each of 16 rows (with the 32x32x16 shape it would be 32 bytes
-// from 32 rows, which halves the rate HBM delivers).
-// Only the token tile (shared by the 8 waves) is staged in LDS, double-buffered.
+// consecutive K values; each weight byte is loaded once per work group.
+// The token tile (shared by the 8 waves) is staged in LDS, double-buffered.
 // Loads run kS - 1 K steps ahead in a ring of kS register sets (kS = 4 in both launches
 // below: three steps, 96 KiB of weights per compute unit, in flight); the K loop is
 // unrolled by kS so that every set is a fixed group of registers and each wait covers
@@ -190,22 +188,29 @@ constexpr int kWStride = kBK + 8;
 // block count every block was its own branch, and each MFMA pair waited for its own LDS
 // read). Blocks past the tile's last token are not computed.
 //
-// Weights reach the MFMA operand registers one of two ways:
-//  * direct (kRowLoads false): each lane loads its own operand pieces; a load instruction
-//    reads 64 bytes from each of 16 rows;
-//  * row-contiguous (kRowLoads true): load instruction i reads the wave's rows 8i .. 8i+7,
-//    128 bytes (one K step) of each, and the wave passes them through its own LDS region
-//    (written, then read back in the operand layout; no other wave touches it, so no
-//    barrier). Each instruction then touches 8 whole cache lines instead of halves of 16,
-//    which halves the L1 requests per weight byte; the down projection ran 13 % faster
-//    this way (223 -> 194 us per Mixtral-shaped layer), gate/up no faster.
-template <int kS, int kNB, int kAN, int kThr, int NMB, bool kRowLoads>
+// Weights reach the MFMA operand registers row-contiguously: load instruction i reads the
+// wave's rows 8i .. 8i+7, 128 bytes (one K step) of each, with the nontemporal hint, and
+// the wave passes them through its own LDS region (written, then read back in the
+// operand layout; no other wave touches it, so no barrier). Each instruction touches 8
+// whole cache lines, where loading each lane's operand pieces directly touches halves of
+// 16: half the L1 requests per weight byte, and whole lines for the nontemporal hint (with
+// half lines it fetched each line twice). The down projection ran 13 % faster this way
+// (223 -> 194 us per Mixtral-shaped layer); gate/up needs it together with kStagger.
+//
+// kStagger (gate/up): each work group starts its K walk at its own step (block id x 7
+// mod the step count) and wraps around, so work groups running at the same time read
+// different 128-byte columns of rows 8 KiB apart instead of the same one. Together with the
+// row-contiguous loads this took gate/up from 414 to 400 us per Mixtral-shaped layer in a
+// same-box A/B; either alone was neutral or slower, and the stagger slowed down (205 ->
+// 208 us), which keeps its fixed K order.
+template <int kS, int kNB, int kAN, int kThr, int NMB, bool kStagger>
 __device__ __forceinline__ void gemm_k_loop(uint16_t (*lds_a)[kTileM * kLdsStride], const uint16_t *const (&asrc)[kAN],
-                                            const uint16_t *const (&bsrc)[kRowLoads ? 2 * kNB : kNB],
-                                            uint16_t *lds_w, int nsteps, floatx4_t (&acc)[kMBlocks][kNB])
+                                            const uint16_t *const (&bsrc)[2 * kNB], uint16_t *lds_w, int nsteps,
+                                            floatx4_t (&acc)[kMBlocks][kNB])
 {
-    static_assert(!kRowLoads || kBK == 64, "row-contiguous weight loads cover 128 bytes of a row per step");
-    constexpr int kLB = kRowLoads ? 2 * kNB : kNB * kKBlocks;   // weight loads per lane per step
+    const int kstag = kStagger ? (int)(blockIdx.x * 7u % (unsigned)nsteps) : 0;
+    static_assert(kBK == 64, "row-contiguous weight loads cover 128 bytes of a row per step");
+    constexpr int kLB = 2 * kNB;   // weight loads per lane per step
     // only the NMB token blocks that hold tokens are staged (the first kAL of the thread's
     // kAN chunks): a tile of 128 tokens stages 128 rows per step, not 192
     constexpr int kChunks = NMB * 16 * kRowChunks;
@@ -213,20 +218,14 @@ __device__ __forceinline__ void gemm_k_loop(uint16_t (*lds_a)[kTileM * kLdsStrid
     static_assert(kAL <= kAN, "staged chunks within the tile's");
     const int tid = threadIdx.x, lane = tid & 63;
     u32x4_t ra[kS][kAL], rb[kS][kLB];
-    u32x4_t rt[kRowLoads ? kNB * kKBlocks : 1];                 // operand pieces after the LDS pass
+    u32x4_t rt[kNB * kKBlocks];                                  // operand pieces after the LDS pass
 #define MOE_LOAD(set, step)                                                                           \
     do {                                                                                              \
-        const int ko_ = min((step), nsteps - 1) * kBK;                                                \
+        const int ko_ = ((min((step), nsteps - 1) + kstag) % nsteps) * kBK;                           \
         _Pragma("unroll") for (int i = 0; i < kAL; ++i) ra[set][i] =                                \
             *reinterpret_cast<const u32x4_t *>(asrc[i] + ko_);                                        \
-        if constexpr (kRowLoads) {                                                                    \
-            _Pragma("unroll") for (int i = 0; i < kLB; ++i) rb[set][i] =                              \
-                __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(bsrc[i] + ko_));         \
-        } else {                                                                                      \
-            _Pragma("unroll") for (int nb = 0; nb < kNB; ++nb)                                        \
-            _Pragma("unroll") for (int kb = 0; kb < kKBlocks; ++kb) rb[set][nb * kKBlocks + kb] =     \
-                *reinterpret_cast<const u32x4_t *>(bsrc[nb] + ko_ + 32 * kb);                         \
-        }                                                                                             \
+        _Pragma("unroll") for (int i = 0; i < kLB; ++i) rb[set][i] =                                  \
+            __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(bsrc[i] + ko_));             \
     } while (0)
 #define MOE_STASH(set, buf)                                                                           \
     do {                                                                                              \
@@ -236,17 +235,14 @@ __device__ __forceinline__ void gemm_k_loop(uint16_t (*lds_a)[kTileM * kLdsStrid
                 *reinterpret_cast<u32x4_t *>(&lds_a[buf][(c_ / kRowChunks) * kLdsStride + (c_ % kRowChunks) * 8]) = ra[set][i]; \
         }                                                                                             \
     } while (0)
-    // row-contiguous path: rows 8i + lane/8 in, operand pieces (row 16 nb + lane mod 16,
-    // K 32 kb + 8 (lane / 16)) out
+    // rows 8i + lane/8 in, operand pieces (row 16 nb + lane mod 16, K 32 kb + 8 (lane / 16)) out
 #define MOE_TRANSPOSE(set)                                                                            \
     do {                                                                                              \
-        if constexpr (kRowLoads) {                                                                    \
-            _Pragma("unroll") for (int i = 0; i < kLB; ++i)                                           \
-                *reinterpret_cast<u32x4_t *>(&lds_w[(8 * i + (lane >> 3)) * kWStride + (lane & 7) * 8]) = rb[set][i]; \
-            _Pragma("unroll") for (int nb = 0; nb < kNB; ++nb)                                        \
-            _Pragma("unroll") for (int kb = 0; kb < kKBlocks; ++kb) rt[nb * kKBlocks + kb] =          \
-                *reinterpret_cast<const u32x4_t *>(&lds_w[(16 * nb + (lane & 15)) * kWStride + kb * 32 + 8 * (lane >> 4)]); \
-        }                                                                                             \
+        _Pragma("unroll") for (int i = 0; i < kLB; ++i)                                               \
+            *reinterpret_cast<u32x4_t *>(&lds_w[(8 * i + (lane >> 3)) * kWStride + (lane & 7) * 8]) = rb[set][i]; \
+        _Pragma("unroll") for (int nb = 0; nb < kNB; ++nb)                                            \
+        _Pragma("unroll") for (int kb = 0; kb < kKBlocks; ++kb) rt[nb * kKBlocks + kb] =              \
+            *reinterpret_cast<const u32x4_t *>(&lds_w[(16 * nb + (lane & 15)) * kWStride + kb * 32 + 8 * (lane >> 4)]); \
     } while (0)
 #define MOE_MMA(set, buf)                                                                             \
     do {                                                                                              \
@@ -256,7 +252,7 @@ __device__ __forceinline__ void gemm_k_loop(uint16_t (*lds_a)[kTileM * kLdsStrid
                     &lds_a[buf][(m * 16 + (lane & 15)) * kLdsStride + kb * 32 + 8 * (lane >> 4)]);     \
                 _Pragma("unroll") for (int nb = 0; nb < kNB; ++nb) acc[m][nb] =                       \
                     __builtin_amdgcn_mfma_f32_16x16x32_bf16(                                          \
-                        a_, __builtin_bit_cast(bf16x8_t, kRowLoads ? rt[nb * kKBlocks + kb] : rb[set][nb * kKBlocks + kb]), \
+                        a_, __builtin_bit_cast(bf16x8_t, rt[nb * kKBlocks + kb]),                     \
                         acc[m][nb], 0, 0, 0);                                                         \
             }                                                                                         \
         }                                                                                             \
@@ -322,9 +318,8 @@ __global__ __launch_bounds__(kWaves * 64) void k_moe_gemm(GemmArgs g)
 {
     constexpr int kThr = kWaves * 64;
     constexpr int kAN = (kTileM * kRowChunks + kThr - 1) / kThr;   // token-tile 16-byte chunks per thread per step
-    constexpr bool kRowLoads = !kGateUp;                // row-contiguous weight loads for down
     __shared__ uint16_t lds_a[2][kTileM * kLdsStride];
-    __shared__ uint16_t lds_w[kRowLoads ? kWaves : 1][kRowLoads ? 16 * kNB * kWStride : 8];
+    __shared__ uint16_t lds_w[kWaves][16 * kNB * kWStride];
 
     const int K = kGateUp ? g.d : g.f;
     int e, mt, nt, ks = 0, kparts = g.ksplit;
@@ -378,19 +373,21 @@ __global__ __launch_bounds__(kWaves * 64) void k_moe_gemm(GemmArgs g)
     const uint16_t *w = reinterpret_cast<const uint16_t *>(g.pool + (uint64_t)e * g.slab_stride);
 
     static_assert(!kGateUp || kNB == 2, "gate/up pairs a W1 block with a W3 block");
-    // this lane's weight rows (MFMA column lane mod 16 of each column block) and K offset;
-    // for row-contiguous loads, row 8i + lane / 8 of the wave's rows at K offset 8 (lane mod 8)
-    const uint16_t *bsrc[kRowLoads ? 2 * kNB : kNB];
-    if constexpr (kRowLoads) {
+    // this lane's weight row and K offset for the row-contiguous loads: row 8i + lane / 8 of
+    // the wave's rows, 8 (lane mod 8) elements into the K step
+    const uint16_t *bsrc[2 * kNB];
+    if constexpr (kGateUp) {   // the wave's 16 W1 rows (loads 0, 1), then the same 16 W3 rows (2, 3)
+#pragma unroll
+        for (int i = 0; i < 2 * kNB; ++i) {
+            const size_t wrow = (size_t)nt * (kWaves * 16) + wv * 16 + 8 * (i & 1) + (lane >> 3);
+            bsrc[i] = w + (i >= 2 ? (size_t)g.f * g.d : 0) + wrow * g.d + k0 + 8 * (lane & 7);
+        }
+    } else {
 #pragma unroll
         for (int i = 0; i < 2 * kNB; ++i) {
             const size_t wrow = (size_t)nt * (kWaves * 16 * kNB) + wv * 16 * kNB + 8 * i + (lane >> 3);
             bsrc[i] = w + (size_t)2 * g.f * g.d + wrow * g.f + k0 + 8 * (lane & 7);
         }
-    } else {   // gate/up, direct: W1 rows, then the same W3 rows
-        const size_t wrow = (size_t)nt * (kWaves * 16) + wv * 16 + (lane & 15);
-        bsrc[0] = w + wrow * g.d + k0 + 8 * (lane >> 4);
-        bsrc[1] = w + (size_t)g.f * g.d + wrow * g.d + k0 + 8 * (lane >> 4);
     }
     // token-tile chunks staged by this thread: chunk c = tid + kThr i is row c / kRowChunks, column
     // c % kRowChunks (chunks past the tile, when the threads do not divide it, load row 0 and are not stored)
@@ -413,7 +410,7 @@ __global__ __launch_bounds__(kWaves * 64) void k_moe_gemm(GemmArgs g)
     // One copy of the K loop per token-block count, chosen once per work group.
     switch (nmb) {
 #define MOE_NMB_CASE(N) \
-    case N: gemm_k_loop<kS, kNB, kAN, kThr, N, kRowLoads>(lds_a, asrc, bsrc, lds_w[kRowLoads ? wv : 0], nsteps, acc); \
+    case N: gemm_k_loop<kS, kNB, kAN, kThr, N, kGateUp>(lds_a, asrc, bsrc, lds_w[wv], nsteps, acc); \
         break;
         MOE_NMB_CASE(1) MOE_NMB_CASE(2) MOE_NMB_CASE(3) MOE_NMB_CASE(4) MOE_NMB_CASE(5) MOE_NMB_CASE(6)
         MOE_NMB_CASE(7) MOE_NMB_CASE(8) MOE_NMB_CASE(9) MOE_NMB_CASE(10) MOE_NMB_CASE(11) MOE_NMB_CASE(12)
