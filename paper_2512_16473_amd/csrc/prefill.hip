@@ -147,7 +147,7 @@ struct GemmArgs {
     int spread;               // 1: item b is simply the b-th (expert, m, n, k) item
     int tail;                 // gate/up, expert-per-XCD layout: split the last partial round over K
     int slots;                // tail: work groups resident per XCD (<= kMaxTailSlots)
-    float *part;              // tail: fp32 (g, u) partial sums [8][slots][kTileM][2 * 16 kWaves]
+    float *part;              // tail: fp32 (g, u) partial sums [8][slots][kTileM][2 kGuCols]
     uint16_t *h;              // gate/up output, bf16 [P][f]
     float *yp;                // down output, fp32 [ksplit][P][d]
 };
@@ -156,24 +156,33 @@ struct GemmArgs {
 // staging buffer: each wave loads its own weight rows and passes them through its own
 // LDS region into the operand layout (see gemm_k_loop).
 //
-// A work group (8 waves) owns up to 192 tokens of one expert and 128 kNB weight rows; each
-// wave owns 16 kNB of the weight rows (kNB 16-row MFMA column blocks) and all the tokens
-// (twelve 16-row blocks). In v_mfma_f32_16x16x32_bf16 the B operand of lane l is 8
-// consecutive K values of column l mod 16, the four lanes l mod 16 + 16 i covering 32
-// consecutive K values; each weight byte is loaded once per work group.
-// The token tile (shared by the 8 waves) is staged in LDS, double-buffered.
-// Loads run kS - 1 K steps ahead in a ring of kS register sets (kS = 4 in both launches
-// below: three steps, 96 KiB of weights per compute unit, in flight); the K loop is
-// unrolled by kS so that every set is a fixed group of registers and each wait covers
-// exactly the oldest set. All loads are unconditional: token rows past the tile re-read row 0 (their
-// outputs are dropped) and steps past the end re-read the last step.
+// A work group (kGWaves waves) owns up to 192 tokens of one expert and a tile of weight
+// rows: for gate/up kGuCols columns of H (that many W1 rows and the same W3 rows), for
+// down 256 (or 128) rows of W2. Each wave owns kNB 16-row MFMA column blocks of them (for
+// gate/up the first kNB/2 are W1 blocks and the rest the matching W3 blocks, so the gate
+// and up values of an output sit in the same lane) and all the tokens (twelve 16-row
+// blocks). In v_mfma_f32_16x16x32_bf16 the B operand of lane l is 8 consecutive K values
+// of column l mod 16, the four lanes l mod 16 + 16 i covering 32 consecutive K values;
+// each weight byte is loaded once per work group. The token tile (shared by the waves) is
+// staged in LDS, double-buffered.
 //
-// gate/up: a wave's two column blocks are 16 W1 rows and the same 16 W3 rows, so the gate
-// and up values of an output sit in the same lane. down: kNB blocks of 16 consecutive W2
-// rows (kNB = 1 when d is not a multiple of 256); K = f is split in ksplit parts that write
-// separate fp32 partial sums.
+// Weight loads run kS - 1 K steps ahead in a ring of kS register sets (kS = 3 below), the
+// token loads one step ahead in a ring of two; the K loop is unrolled so that every set is
+// a fixed group of registers. All loads are unconditional: token rows past the tile
+// re-read row 0 (their outputs are dropped) and steps past the end re-read the last step.
+// K = f of the down projection is split in ksplit parts that write separate fp32 partial
+// sums.
+//
+// Eight waves of 32 weight rows each (kNB = 2) and four waves of 64 rows (kNB = 4, one
+// wave per SIMD, accumulators in AGPRs, half the LDS reads of token operands per MFMA)
+// ran within 2 % of each other on the Mixtral-shaped layer; a per-wave clock trace shows
+// the K step bound by the LDS reads of the token operands and the MFMAs that wait for
+// them, not by the weight stream (the step takes as long with the weight loads removed).
 typedef float floatx4_t __attribute__((ext_vector_type(4)));
 constexpr int kGWaves = 8;                             // waves per work group of the launches below
+constexpr int kGuCols = 128;                           // H columns per gate/up work group
+constexpr int kGuNB = 2 * kGuCols / (16 * kGWaves);    // gate/up column blocks per wave (W1 and W3 halves)
+constexpr int kDnNB = 256 / (16 * kGWaves);            // down column blocks per wave (256-row tiles)
 constexpr int kMBlocks = 12;                           // 16-token blocks per tile
 constexpr int kTileM = kMBlocks * 16;                  // 192 tokens
 constexpr int kKBlocks = kBK / 32;                     // MFMA K blocks per step
@@ -183,10 +192,12 @@ constexpr int kKBlocks = kBK / 32;                     // MFMA K blocks per step
 constexpr int kWStride = kBK + 8;
 
 // The K loop of k_moe_gemm for a tile of NMB 16-token blocks. NMB is a compile-time
-// constant so the MFMA sequence of a step has no branches: the compiler can then issue
-// the LDS reads of the token blocks ahead of the MFMAs that use them (with a run-time
-// block count every block was its own branch, and each MFMA pair waited for its own LDS
-// read). Blocks past the tile's last token are not computed.
+// constant so the MFMA sequence of a step has no branches, and the LDS reads of the
+// token blocks are issued kAP MFMA items ahead of their use (with a run-time block count
+// every block was its own branch, and each MFMA pair waited for its own LDS read; with a
+// constant count but no pinned order, the compiler still read each block just before its
+// MFMAs: 632 against 601 us per Mixtral-shaped layer with the lookahead). Blocks past the
+// tile's last token are not computed.
 //
 // Weights reach the MFMA operand registers row-contiguously: load instruction i reads the
 // wave's rows 8i .. 8i+7, 128 bytes (one K step) of each, with the nontemporal hint, and
@@ -203,7 +214,7 @@ constexpr int kWStride = kBK + 8;
 // row-contiguous loads this took gate/up from 414 to 400 us per Mixtral-shaped layer in a
 // same-box A/B; either alone was neutral or slower, and the stagger slowed down (205 ->
 // 208 us), which keeps its fixed K order.
-template <int kS, int kNB, int kAN, int kThr, int NMB, bool kStagger>
+template <int kS, int kAP, int kNB, int kAN, int kThr, int NMB, bool kStagger>
 __device__ __forceinline__ void gemm_k_loop(uint16_t (*lds_a)[kTileM * kLdsStride], const uint16_t *const (&asrc)[kAN],
                                             const uint16_t *const (&bsrc)[2 * kNB], uint16_t *lds_w, int nsteps,
                                             floatx4_t (&acc)[kMBlocks][kNB])
@@ -211,26 +222,33 @@ __device__ __forceinline__ void gemm_k_loop(uint16_t (*lds_a)[kTileM * kLdsStrid
     const int kstag = kStagger ? (int)(blockIdx.x * 7u % (unsigned)nsteps) : 0;
     static_assert(kBK == 64, "row-contiguous weight loads cover 128 bytes of a row per step");
     constexpr int kLB = 2 * kNB;   // weight loads per lane per step
+    constexpr int kSA = 2;         // token register sets: one step ahead
+    constexpr int kU = kS % kSA == 0 ? kS : kS * kSA;   // unroll: both rings at fixed registers
     // only the NMB token blocks that hold tokens are staged (the first kAL of the thread's
     // kAN chunks): a tile of 128 tokens stages 128 rows per step, not 192
     constexpr int kChunks = NMB * 16 * kRowChunks;
     constexpr int kAL = (kChunks + kThr - 1) / kThr;
     static_assert(kAL <= kAN, "staged chunks within the tile's");
     const int tid = threadIdx.x, lane = tid & 63;
-    u32x4_t ra[kS][kAL], rb[kS][kLB];
+    u32x4_t ra[kSA][kAL], rb[kS][kLB];
     u32x4_t rt[kNB * kKBlocks];                                  // operand pieces after the LDS pass
-#define MOE_LOAD(set, step)                                                                           \
+#define MOE_KOFF(step) (((min((step), nsteps - 1) + kstag) % nsteps) * kBK)
+#define MOE_LOAD_A(set, step)                                                                         \
     do {                                                                                              \
-        const int ko_ = ((min((step), nsteps - 1) + kstag) % nsteps) * kBK;                           \
-        _Pragma("unroll") for (int i = 0; i < kAL; ++i) ra[set][i] =                                \
+        const int ko_ = MOE_KOFF(step);                                                               \
+        _Pragma("unroll") for (int i = 0; i < kAL; ++i) ra[set][i] =                                  \
             *reinterpret_cast<const u32x4_t *>(asrc[i] + ko_);                                        \
+    } while (0)
+#define MOE_LOAD_W(set, step)                                                                         \
+    do {                                                                                              \
+        const int ko_ = MOE_KOFF(step);                                                               \
         _Pragma("unroll") for (int i = 0; i < kLB; ++i) rb[set][i] =                                  \
             __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(bsrc[i] + ko_));             \
     } while (0)
 #define MOE_STASH(set, buf)                                                                           \
     do {                                                                                              \
-        _Pragma("unroll") for (int i = 0; i < kAL; ++i) {                                           \
-            const int c_ = tid + kThr * i;                                                       \
+        _Pragma("unroll") for (int i = 0; i < kAL; ++i) {                                             \
+            const int c_ = tid + kThr * i;                                                            \
             if (kChunks % kThr == 0 || c_ < kChunks)                                                  \
                 *reinterpret_cast<u32x4_t *>(&lds_a[buf][(c_ / kRowChunks) * kLdsStride + (c_ % kRowChunks) * 8]) = ra[set][i]; \
         }                                                                                             \
@@ -244,39 +262,56 @@ __device__ __forceinline__ void gemm_k_loop(uint16_t (*lds_a)[kTileM * kLdsStrid
         _Pragma("unroll") for (int kb = 0; kb < kKBlocks; ++kb) rt[nb * kKBlocks + kb] =              \
             *reinterpret_cast<const u32x4_t *>(&lds_w[(16 * nb + (lane & 15)) * kWStride + kb * 32 + 8 * (lane >> 4)]); \
     } while (0)
-#define MOE_MMA(set, buf)                                                                             \
+    // token operand of MFMA item j (K block j / NMB, token block j mod NMB)
+#define MOE_AREAD(j, buf)                                                                             \
+    (*reinterpret_cast<const bf16x8_t *>(                                                             \
+        &lds_a[buf][(((j) % NMB) * 16 + (lane & 15)) * kLdsStride + ((j) / NMB) * 32 + 8 * (lane >> 4)]))
+    // The token operands are read kAP items ahead of their MFMAs, in a ring of kAP registers,
+    // and the order is pinned (left to itself the compiler read each operand just before its
+    // MFMA pair and waited for it, so the LDS latency was paid once per token block).
+#define MOE_MMA(buf)                                                                                  \
     do {                                                                                              \
-        _Pragma("unroll") for (int kb = 0; kb < kKBlocks; ++kb) {                                     \
-            _Pragma("unroll") for (int m = 0; m < NMB; ++m) {                                         \
-                const bf16x8_t a_ = *reinterpret_cast<const bf16x8_t *>(                              \
-                    &lds_a[buf][(m * 16 + (lane & 15)) * kLdsStride + kb * 32 + 8 * (lane >> 4)]);     \
-                _Pragma("unroll") for (int nb = 0; nb < kNB; ++nb) acc[m][nb] =                       \
-                    __builtin_amdgcn_mfma_f32_16x16x32_bf16(                                          \
-                        a_, __builtin_bit_cast(bf16x8_t, rt[nb * kKBlocks + kb]),                     \
-                        acc[m][nb], 0, 0, 0);                                                         \
-            }                                                                                         \
+        constexpr int kJ_ = kKBlocks * NMB;                                                           \
+        bf16x8_t aq_[kAP];                                                                            \
+        _Pragma("unroll") for (int j = 0; j < kAP; ++j) if (j < kJ_) aq_[j] = MOE_AREAD(j, buf);      \
+        _Pragma("unroll") for (int j = 0; j < kJ_; ++j) {                                             \
+            const bf16x8_t a_ = aq_[j % kAP];                                                         \
+            if (j + kAP < kJ_) aq_[j % kAP] = MOE_AREAD(j + kAP, buf);                                \
+            _Pragma("unroll") for (int nb = 0; nb < kNB; ++nb) acc[j % NMB][nb] =                     \
+                __builtin_amdgcn_mfma_f32_16x16x32_bf16(                                              \
+                    a_, __builtin_bit_cast(bf16x8_t, rt[nb * kKBlocks + j / NMB]),                    \
+                    acc[j % NMB][nb], 0, 0, 0);                                                       \
+            __builtin_amdgcn_sched_barrier(0);                                                        \
         }                                                                                             \
     } while (0)
 
+    // Step t: the tokens of step t + 1 are loaded first, then the weights of step
+    // t + kS - 1; the token stash at the end of the step waits for the former, and since
+    // loads complete in issue order that also covers every weight set issued before it.
+    MOE_LOAD_A(0, 0);
 #pragma unroll
-    for (int p = 0; p < kS - 1; ++p) MOE_LOAD(p, p);
+    for (int p = 0; p < kS - 1; ++p) MOE_LOAD_W(p, p);
     MOE_STASH(0, 0);
     __syncthreads();
-    for (int s = 0; s < nsteps; s += kS) {
+    for (int s = 0; s < nsteps; s += kU) {
 #pragma unroll
-        for (int u = 0; u < kS; ++u) {
+        for (int u = 0; u < kU; ++u) {
             if (s + u >= nsteps) break;
-            MOE_TRANSPOSE(u);
-            MOE_LOAD((u + kS - 1) % kS, s + u + kS - 1);
-            MOE_MMA(u, (s + u) & 1);
-            MOE_STASH((u + 1) % kS, (s + u + 1) & 1);
+            MOE_TRANSPOSE(u % kS);
+            MOE_LOAD_A((u + 1) % kSA, s + u + 1);
+            MOE_LOAD_W((u + kS - 1) % kS, s + u + kS - 1);
+            MOE_MMA((s + u) & 1);
+            MOE_STASH((u + 1) % kSA, (s + u + 1) & 1);
             __syncthreads();
         }
     }
-#undef MOE_LOAD
+#undef MOE_KOFF
+#undef MOE_LOAD_A
+#undef MOE_LOAD_W
 #undef MOE_STASH
 #undef MOE_TRANSPOSE
 #undef MOE_MMA
+#undef MOE_AREAD
 }
 
 // Gate/up tail split (expert-per-XCD layout). The live tiles of XCD x (its experts x,
@@ -372,15 +407,16 @@ __global__ __launch_bounds__(kWaves * 64) void k_moe_gemm(GemmArgs g)
     const int nmb = (rows + 15) >> 4;                  // token blocks holding tokens of this tile
     const uint16_t *w = reinterpret_cast<const uint16_t *>(g.pool + (uint64_t)e * g.slab_stride);
 
-    static_assert(!kGateUp || kNB == 2, "gate/up pairs a W1 block with a W3 block");
+    static_assert(!kGateUp || (kNB % 2 == 0 && kWaves * 8 * kNB == kGuCols),
+                  "gate/up pairs each W1 block with a W3 block over kGuCols columns");
     // this lane's weight row and K offset for the row-contiguous loads: row 8i + lane / 8 of
     // the wave's rows, 8 (lane mod 8) elements into the K step
     const uint16_t *bsrc[2 * kNB];
-    if constexpr (kGateUp) {   // the wave's 16 W1 rows (loads 0, 1), then the same 16 W3 rows (2, 3)
+    if constexpr (kGateUp) {   // the wave's 8 kNB W1 rows (loads 0 .. kNB-1), then the same W3 rows
 #pragma unroll
         for (int i = 0; i < 2 * kNB; ++i) {
-            const size_t wrow = (size_t)nt * (kWaves * 16) + wv * 16 + 8 * (i & 1) + (lane >> 3);
-            bsrc[i] = w + (i >= 2 ? (size_t)g.f * g.d : 0) + wrow * g.d + k0 + 8 * (lane & 7);
+            const size_t wrow = (size_t)nt * kGuCols + wv * 8 * kNB + 8 * (i % kNB) + (lane >> 3);
+            bsrc[i] = w + (i >= kNB ? (size_t)g.f * g.d : 0) + wrow * g.d + k0 + 8 * (lane & 7);
         }
     } else {
 #pragma unroll
@@ -408,9 +444,10 @@ __global__ __launch_bounds__(kWaves * 64) void k_moe_gemm(GemmArgs g)
         for (int nb = 0; nb < kNB; ++nb) acc[m][nb] = floatx4_t{0.f, 0.f, 0.f, 0.f};
 
     // One copy of the K loop per token-block count, chosen once per work group.
+    constexpr int kTokAhead = 6;   // token operand reads kept ahead of the MFMAs
     switch (nmb) {
 #define MOE_NMB_CASE(N) \
-    case N: gemm_k_loop<kS, kNB, kAN, kThr, N, kGateUp>(lds_a, asrc, bsrc, lds_w[wv], nsteps, acc); \
+    case N: gemm_k_loop<kS, kTokAhead, kNB, kAN, kThr, N, kGateUp>(lds_a, asrc, bsrc, lds_w[wv], nsteps, acc); \
         break;
         MOE_NMB_CASE(1) MOE_NMB_CASE(2) MOE_NMB_CASE(3) MOE_NMB_CASE(4) MOE_NMB_CASE(5) MOE_NMB_CASE(6)
         MOE_NMB_CASE(7) MOE_NMB_CASE(8) MOE_NMB_CASE(9) MOE_NMB_CASE(10) MOE_NMB_CASE(11) MOE_NMB_CASE(12)
@@ -421,7 +458,7 @@ __global__ __launch_bounds__(kWaves * 64) void k_moe_gemm(GemmArgs g)
     // Output element r of a 16x16 block sits at row 4*(lane/16) + r, column lane%16.
     if constexpr (kGateUp) {
         if (tail_v >= 0) {   // a K part of a split tile: its fp32 (g, u) sums, added by k_tail_combine
-            constexpr int kCols = 2 * kWaves * 16;   // g columns, then u columns
+            constexpr int kCols = 2 * kGuCols;   // g columns, then u columns
             float *mine = g.part + ((size_t)xcd * g.slots + tail_v) * kTileM * kCols;
 #pragma unroll
             for (int m = 0; m < kMBlocks; ++m)
@@ -429,8 +466,12 @@ __global__ __launch_bounds__(kWaves * 64) void k_moe_gemm(GemmArgs g)
                 for (int r = 0; r < 4; ++r) {
                     const int tr = m * 16 + 4 * (lane >> 4) + r;
                     if (tr >= rows) continue;
-                    mine[tr * kCols + wv * 16 + (lane & 15)] = acc[m][0][r];
-                    mine[tr * kCols + kWaves * 16 + wv * 16 + (lane & 15)] = acc[m][kNB - 1][r];
+#pragma unroll
+                    for (int nb = 0; nb < kNB / 2; ++nb) {
+                        const int c = wv * 8 * kNB + 16 * nb + (lane & 15);
+                        mine[tr * kCols + c] = acc[m][nb][r];
+                        mine[tr * kCols + kGuCols + c] = acc[m][nb + kNB / 2][r];
+                    }
                 }
             return;
         }
@@ -443,9 +484,12 @@ __global__ __launch_bounds__(kWaves * 64) void k_moe_gemm(GemmArgs g)
             const int tr = m * 16 + 4 * (lane >> 4) + r;
             if (tr >= rows) continue;
             if constexpr (kGateUp) {
-                const float gv = acc[m][0][r], uv = acc[m][kNB - 1][r];
-                const float hv = gv / (1.0f + expf(-gv)) * uv;
-                g.h[(size_t)(row0 + tr) * g.f + nt * (kWaves * 16) + wv * 16 + (lane & 15)] = f2bf(hv);
+#pragma unroll
+                for (int nb = 0; nb < kNB / 2; ++nb) {
+                    const float gv = acc[m][nb][r], uv = acc[m][nb + kNB / 2][r];
+                    const float hv = gv / (1.0f + expf(-gv)) * uv;
+                    g.h[(size_t)(row0 + tr) * g.f + nt * kGuCols + wv * 8 * kNB + 16 * nb + (lane & 15)] = f2bf(hv);
+                }
             } else {
                 float *dst = g.yp + ((size_t)ks * P + row0 + tr) * g.d + nt * (kWaves * 16 * kNB) + wv * 16 * kNB +
                              (lane & 15);
@@ -463,8 +507,8 @@ __global__ __launch_bounds__(kWaves * 64) void k_moe_gemm(GemmArgs g)
 constexpr int kTailRows = 16;
 __global__ __launch_bounds__(kThreads) void k_tail_combine(GemmArgs g)
 {
-    constexpr int kCols = 2 * kGWaves * 16;   // g columns, then u columns
-    constexpr int kQuads = kGWaves * 16 / 4;  // 4-column groups of the tile's 128 columns
+    constexpr int kCols = 2 * kGuCols;   // g columns, then u columns
+    constexpr int kQuads = kGuCols / 4;  // 4-column groups of the tile's columns
     const int xcd = blockIdx.x % kXcds;
     const int i = (blockIdx.x / kXcds) % g.slots;
     const int rb = blockIdx.x / kXcds / g.slots;
@@ -489,7 +533,7 @@ __global__ __launch_bounds__(kThreads) void k_tail_combine(GemmArgs g)
         uint2 o;
         o.x = f2bf(gv.x / (1.0f + expf(-gv.x)) * uv.x) | ((uint32_t)f2bf(gv.y / (1.0f + expf(-gv.y)) * uv.y) << 16);
         o.y = f2bf(gv.z / (1.0f + expf(-gv.z)) * uv.z) | ((uint32_t)f2bf(gv.w / (1.0f + expf(-gv.w)) * uv.w) << 16);
-        *reinterpret_cast<uint2 *>(g.h + (size_t)(row0 + tr) * g.f + nt * (kGWaves * 16) + col) = o;
+        *reinterpret_cast<uint2 *>(g.h + (size_t)(row0 + tr) * g.f + nt * kGuCols + col) = o;
     }
 }
 
@@ -539,7 +583,7 @@ struct PrefillWs {
 bool spread_layout(int n, int k, int T) { return (int64_t)T * k < (int64_t)kSpreadTokens * n; }
 
 // fp32 (g, u) partial sums of the gate/up tiles split over K: [8][kMaxTailSlots][kTileM][2 * 128]
-constexpr size_t kPartBytes = (size_t)kXcds * kMaxTailSlots * kTileM * 2 * kGWaves * 16 * sizeof(float);
+constexpr size_t kPartBytes = (size_t)kXcds * kMaxTailSlots * kTileM * 2 * kGuCols * sizeof(float);
 
 size_t layout(int d, int f, int n, int k, int T, uint8_t *base, PrefillWs *ws)
 {
@@ -616,13 +660,13 @@ hipError_t launch_prefill(const PrefillPlan &P, const float *X, float *OUT, int3
 
     // gate/up: each work group covers 128 columns of H (128 W1 rows + the same 128 W3 rows), K = d
     g.a = ws.xb;
-    g.ntiles = P.f / (kGWaves * 16);
+    g.ntiles = P.f / kGuCols;
     g.ksplit = 1;
     g.per_xcd = groups * g.mtiles * g.ntiles * g.ksplit;
     // Tail splitting (expert-per-XCD layout): the rounds of resident work groups per XCD
     // decide which tiles are split.
     static int gu_occ = -1;
-    if (gu_occ < 0 && (hipOccupancyMaxActiveBlocksPerMultiprocessor(&gu_occ, k_moe_gemm<true, 4, 2, kGWaves>,
+    if (gu_occ < 0 && (hipOccupancyMaxActiveBlocksPerMultiprocessor(&gu_occ, k_moe_gemm<true, 3, kGuNB, kGWaves>,
                                                                      kGWaves * 64, 0) != hipSuccess || gu_occ < 1)) {
         (void)hipGetLastError();
         gu_occ = 0;
@@ -635,7 +679,7 @@ hipError_t launch_prefill(const PrefillPlan &P, const float *X, float *OUT, int3
     // live tiles plus one round of parts
     const int gu_per_xcd = g.tail ? g.per_xcd + g.slots : g.per_xcd;
     const int gu_grid = g.spread ? grid_of(g) : kXcds * gu_per_xcd;
-    hipLaunchKernelGGL((k_moe_gemm<true, 4, 2, kGWaves>), dim3(gu_grid), dim3(kGWaves * 64), 0, s, g);
+    hipLaunchKernelGGL((k_moe_gemm<true, 3, kGuNB, kGWaves>), dim3(gu_grid), dim3(kGWaves * 64), 0, s, g);
     if ((e = hipGetLastError()) != hipSuccess) return e;
     if (g.tail) {
         hipLaunchKernelGGL(k_tail_combine, dim3(kXcds * g.slots * (kTileM / kTailRows)), dim3(kThreads), 0, s, g);
@@ -646,11 +690,11 @@ hipError_t launch_prefill(const PrefillPlan &P, const float *X, float *OUT, int3
     g.tail = 0;
     g.a = ws.h;
     g.ksplit = down_splits(P.f);
-    const bool wide = P.d % (kGWaves * 32) == 0;
-    g.ntiles = P.d / (kGWaves * 16 * (wide ? 2 : 1));
+    const bool wide = P.d % 256 == 0;
+    g.ntiles = P.d / (wide ? 256 : 128);
     g.per_xcd = groups * g.mtiles * g.ntiles * g.ksplit;
-    if (wide) hipLaunchKernelGGL((k_moe_gemm<false, 4, 2, kGWaves>), dim3(grid_of(g)), dim3(kGWaves * 64), 0, s, g);
-    else hipLaunchKernelGGL((k_moe_gemm<false, 4, 1, kGWaves>), dim3(grid_of(g)), dim3(kGWaves * 64), 0, s, g);
+    if (wide) hipLaunchKernelGGL((k_moe_gemm<false, 3, kDnNB, kGWaves>), dim3(grid_of(g)), dim3(kGWaves * 64), 0, s, g);
+    else hipLaunchKernelGGL((k_moe_gemm<false, 3, kDnNB / 2, kGWaves>), dim3(grid_of(g)), dim3(kGWaves * 64), 0, s, g);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     const int nparts = (P.d + 4 * kThreads - 1) / (4 * kThreads);
