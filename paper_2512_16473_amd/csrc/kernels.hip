@@ -16,6 +16,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <mutex>
 
 #include "moe.h"
@@ -590,13 +591,15 @@ __global__ __launch_bounds__(kRouteBlkThreads) void k_router_blk(const float *x,
     }
 }
 
-// Resident blocks per CU of a kernel (cached by the caller). If the runtime cannot
-// answer, the count is derived from the kernel's register use (512 VGPRs per SIMD
-// lane, one wave per SIMD per 256-thread block), else 2.
+// Resident blocks per CU of a kernel (cached by the caller; concurrent first calls
+// store the same value). If the runtime cannot answer, the count is derived from the
+// kernel's register use (512 VGPRs per SIMD lane, one wave per SIMD per 256-thread
+// block), else 2.
 template <typename K>
-int blocks_per_cu(K kernel, int block, int *cache)
+int blocks_per_cu(K kernel, int block, std::atomic<int> *cache)
 {
-    if (*cache <= 0) {
+    int c = cache->load(std::memory_order_relaxed);
+    if (c <= 0) {
         int b = 0;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, kernel, block, 0) != hipSuccess || b <= 0) {
             (void)hipGetLastError();
@@ -611,9 +614,10 @@ int blocks_per_cu(K kernel, int block, int *cache)
                 (void)hipGetLastError();
             }
         }
-        *cache = b;
+        cache->store(b, std::memory_order_relaxed);
+        c = b;
     }
-    return *cache;
+    return c;
 }
 
 // Launch status: the runtime's last error is cleared before each launch (another
@@ -626,7 +630,7 @@ hipError_t launch_gate_up_cpl(const FfnParams &p, int items, hipStream_t s, hipE
     // Up to 4 x the resident work groups (more waves, each with a few row pairs, hide the
     // load latency better than fewer longer-lived ones), fewer while that would leave
     // under two row pairs per wave (each wave loads x before its first row).
-    static int occ = 0;
+    static std::atomic<int> occ{0};
     const int resident = blocks_per_cu(k_gate_up<CPL>, kBlock, &occ) * device_cu_count();
     int cap = resident * 4;
     while (cap > resident && (int64_t)cap * kWavesPerBlock * 2 > items) cap /= 2;
@@ -695,15 +699,15 @@ hipError_t noalloc_scratch(void **ptr)
 
 int device_cu_count()
 {
-    static int cached[64] = {0};
+    static std::atomic<int> cached[64] = {};   // per device; concurrent first calls store the same value
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-    if (cached[dev] == 0) {
-        int v = 0;
+    int v = cached[dev].load(std::memory_order_relaxed);
+    if (v == 0) {
         if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
-        cached[dev] = v;
+        cached[dev].store(v, std::memory_order_relaxed);
     }
-    return cached[dev];
+    return v;
 }
 
 static size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
@@ -781,7 +785,7 @@ hipError_t launch_ffn_stream(const FfnParams &p, hipStream_t s, const FfnEvents 
     hipError_t e;
     if ((e = launch_gate_up(p, rows_max, s, ev ? ev->gu_start : nullptr, ev ? ev->gu_stop : nullptr)) != hipSuccess)
         return e;
-    static int occ_down = 0;
+    static std::atomic<int> occ_down{0};
     const int blocks = blocks_per_cu(k_down, kBlock, &occ_down) * device_cu_count();
     clear_launch_error();
     if (ev && (ev->dn_start || ev->dn_stop))

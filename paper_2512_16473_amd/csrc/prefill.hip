@@ -25,6 +25,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <atomic>
 
 #include "common.h"
 #include "moe_internal.h"
@@ -665,11 +666,16 @@ hipError_t launch_prefill(const PrefillPlan &P, const float *X, float *OUT, int3
     g.per_xcd = groups * g.mtiles * g.ntiles * g.ksplit;
     // Tail splitting (expert-per-XCD layout): the rounds of resident work groups per XCD
     // decide which tiles are split.
-    static int gu_occ = -1;
-    if (gu_occ < 0 && (hipOccupancyMaxActiveBlocksPerMultiprocessor(&gu_occ, k_moe_gemm<true, 3, kGuNB, kGWaves>,
-                                                                     kGWaves * 64, 0) != hipSuccess || gu_occ < 1)) {
-        (void)hipGetLastError();
-        gu_occ = 0;
+    static std::atomic<int> gu_occ_cache{-1};   // concurrent first calls store the same value
+    int gu_occ = gu_occ_cache.load(std::memory_order_relaxed);
+    if (gu_occ < 0) {
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&gu_occ, k_moe_gemm<true, 3, kGuNB, kGWaves>, kGWaves * 64,
+                                                         0) != hipSuccess ||
+            gu_occ < 1) {
+            (void)hipGetLastError();
+            gu_occ = 0;
+        }
+        gu_occ_cache.store(gu_occ, std::memory_order_relaxed);
     }
     const int slots = std::min(kMaxTailSlots, gu_occ * device_cu_count() / kXcds);
     g.tail = !g.spread && slots >= 2;
