@@ -86,25 +86,36 @@ def test_prefill_small(d, f, n, k, T):
     say("  worst max|err|/RMS vs oracle", worst, "vs bf16-activation reference", worst_b)
 
 
-def test_prefill_mixtral_full_shape():
-    """Config: Mixtral-8x7B-shaped prefill, one 512-token prompt, all 8 experts resident,
-    in the launch configuration the benchmark times (one M tile per expert, the gate/up
-    tail split over K on 8 XCDs): every token's routing and every token's output
-    compared with the oracle."""
+@pytest.mark.parametrize("shape", ["mixtral", "phi", "fine"])
+def test_prefill_full_shape(shape):
+    """Configs: one 512-token prompt through a full-size layer with every expert resident,
+    in the launch configuration the benchmark times, every token's routing and output
+    compared with the oracle.
+    * mixtral (the benchmark's prefill line): one M tile per expert, one expert per XCD,
+      the gate/up tail split in 2 K parts;
+    * phi (d 4096, f 6400, 16 experts top-2): two experts per XCD, 100 gate/up tiles per
+      XCD, the last 4 split in 8 K parts;
+    * fine (d 3584, f 2560, 64 experts top-8, routed experts only): d not a multiple of
+      256 (128-row down tiles) and 64 (token, expert) pairs per expert on average."""
     torch = torch_cuda()
     import paper_2512_16473_amd as moe
-    wl = synth.WORKLOADS["prefill"]
-    d, f, n, k, T = wl.d, wl.f, wl.n, wl.k, wl.T
-    say("prefill mixtral", d, f, n, k, T)
+    if shape == "mixtral":
+        wl = synth.WORKLOADS["prefill"]
+        tag = "prefill"
+    else:
+        wl = synth.WORKLOADS[shape]
+        tag = "prefill-" + shape
+    d, f, n, k, T = wl.d, wl.f, wl.n, wl.k, 512
+    say("prefill", shape, d, f, n, k, T)
     stride = moe.slab_bytes(d, f)
     pool = torch.empty(n * stride, dtype=torch.uint8, device="cuda")
     host = []
     for e in range(n):
         t = pool[e * stride: e * stride + 3 * d * f * 2].view(torch.bfloat16)
-        synth.expert_slab_torch(synth.seed_for(0, "prefill", "expert", 0, e), d, f, wl.w_std, out=t)
+        synth.expert_slab_torch(synth.seed_for(0, tag, "expert", 0, e), d, f, wl.w_std, out=t)
         host.append(t.view(torch.uint8).cpu().numpy().view(np.uint16))
-    wr = synth.router_weights(synth.seed_for(0, "prefill", "router", 0), n, d)
-    X = synth.iid_states(synth.seed_for(0, "prefill", "prompt"), T, d)
+    wr = synth.router_weights(synth.seed_for(0, tag, "router", 0), n, d)
+    X = synth.iid_states(synth.seed_for(0, tag, "prompt"), T, d)
     out, idx, w = _run(torch, X, wr, pool, d, f, n, k)
     oracle.set_threads(min(16, os.cpu_count() or 1))
     sets = []
