@@ -554,6 +554,17 @@ __global__ __launch_bounds__(kRouteBlkThreads) void k_router_blk(const float *x,
 #pragma unroll
     for (int m = 0; m < kPerLane; ++m)
         if (q0 + m * kWave + lane >= nq) xq[m] = make_float4(0, 0, 0, 0);
+    // x for the host: the first wave of each segment writes its slice as soon as it has
+    // it, so the writes cross PCIe while the logits are computed (the system-scope fence
+    // before the sequence number covers them)
+    if (x_host && wv < nseg) {
+        float4 *xh = reinterpret_cast<float4 *>(x_host);
+#pragma unroll
+        for (int m = 0; m < kPerLane; ++m) {
+            const int q = q0 + m * kWave + lane;
+            if (q < nq) xh[q] = xq[m];
+        }
+    }
 #pragma unroll
     for (int u = 0; u < kRouteBlkPerWave; ++u) {
         // one item at a time: keeps the scheduler from widening every loaded value to
@@ -578,12 +589,7 @@ __global__ __launch_bounds__(kRouteBlkThreads) void k_router_blk(const float *x,
         logit[e] = l;
     }
     __syncthreads();
-    if (wv == 0) {
-        select_topk(logit, n, k, lane, idx, wout, mbox);
-    } else if (x_host) {
-        float4 *xh = reinterpret_cast<float4 *>(x_host);
-        for (int q = threadIdx.x - kWave; q < nq; q += kRouteBlkThreads - kWave) xh[q] = x4[q];
-    }
+    if (wv == 0) select_topk(logit, n, k, lane, idx, wout, mbox);
     if (mbox) {
         __threadfence_system();
         __syncthreads();
