@@ -272,22 +272,30 @@ __global__ __launch_bounds__(kBlock) void k_down(FfnParams p)
     }
 }
 
-// out[i] = the compact partials summed in index order (+ y_extra[i]).
+// out[i] = the compact partials summed in index order (+ y_extra[i]). The first kRedU
+// partial rows (the workspace always holds kMaxJobs x smax of them) and y_extra are
+// loaded together with the partial count, so the kernel waits for one round trip
+// rather than for the count and then for the rows; the sum keeps the index order.
+constexpr int kRedU = 8;
+static_assert(kRedU <= kMaxJobs, "rows loaded ahead of the count lie in the partial region");
+
 __global__ __launch_bounds__(kBlock) void k_reduce(FfnParams p, const float *y_extra, float *out)
 {
     const int i = blockIdx.x * kBlock + threadIdx.x;
     if (i >= p.d) return;
-    const int nparts = p.jobslot[kMetaParts];
     const float *src = p.partial + i;
     const size_t ld = (size_t)p.d;
+    float v[kRedU];
+#pragma unroll
+    for (int q = 0; q < kRedU; ++q) v[q] = src[q * ld];
+    const float ye = y_extra ? y_extra[i] : 0.f;
+    const int nparts = p.jobslot[kMetaParts];
     float acc = 0.f;
-    int q = 0;
-    for (; q + 4 <= nparts; q += 4) {
-        const float a = src[q * ld], b = src[(q + 1) * ld], c = src[(q + 2) * ld], e = src[(q + 3) * ld];
-        acc = (((acc + a) + b) + c) + e;
-    }
-    for (; q < nparts; ++q) acc += src[q * ld];
-    if (y_extra) acc += y_extra[i];
+#pragma unroll
+    for (int q = 0; q < kRedU; ++q)
+        if (q < nparts) acc += v[q];
+    for (int q = kRedU; q < nparts; ++q) acc += src[q * ld];
+    if (y_extra) acc += ye;
     out[i] = acc;
 }
 
