@@ -174,15 +174,18 @@ __global__ __launch_bounds__(kBlock) void k_gate_up(FfnParams p)
 }
 
 // True in the one work group of the grid that arrives last at this point. Every work
-// group calls it once, with all its threads; the partial results each wrote before the
-// call are visible to the last one after it returns (device-scope fences around the
-// arrival counter, which the caller zeroed before the launch or the last group resets).
+// group calls it once, with all its threads, after thread 0 alone wrote the group's
+// partial results to global memory; those are visible to the last group after it
+// returns (thread 0's device-scope release before the arrival counter, which the caller
+// zeroed before the launch or the last group resets, and an acquire in every thread of
+// the last group). One release per work group: each writes the XCD's L2 back.
 __device__ __forceinline__ bool arrive_last(unsigned *ticket)
 {
     __shared__ int last;
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) last = atomicAdd(ticket, 1u) == gridDim.x - 1;
+    if (threadIdx.x == 0) {
+        __threadfence();
+        last = atomicAdd(ticket, 1u) == gridDim.x - 1;
+    }
     __syncthreads();
     if (!last) return false;
     __threadfence();
@@ -465,6 +468,7 @@ __global__ __launch_bounds__(kBlock) void k_route1(const float *x, const float *
     const int item = blockIdx.x * kWavesPerBlock + (threadIdx.x >> 6);
     const int nseg = (d + kRouteSeg - 1) / kRouteSeg;
     const int nq = d >> 2;
+    __shared__ double part_l[kWavesPerBlock];
     if (item < n * nseg) {
         const int e = item / nseg;
         const int q0 = (item - e * nseg) * (kRouteSeg / 4);
@@ -489,8 +493,14 @@ __global__ __launch_bounds__(kBlock) void k_route1(const float *x, const float *
             acc += (double)wv[m].w * (double)xv[m].w;
         }
         acc = wave_sum(acc);
-        if (lane == 0) part[item] = acc;
+        if (lane == 0) part_l[threadIdx.x >> 6] = acc;
     }
+    __syncthreads();
+    if (threadIdx.x == 0)   // the group's partials, written by the thread that releases them
+        for (int w = 0; w < kWavesPerBlock; ++w) {
+            const int it = blockIdx.x * kWavesPerBlock + w;
+            if (it < n * nseg) part[it] = part_l[w];
+        }
     if (!arrive_last(ticket)) return;
     __shared__ double logit[MOE_MAX_EXPERTS];
     for (int e = threadIdx.x; e < n; e += kBlock) {
