@@ -133,7 +133,7 @@ def test_cache_sizing_example(golden_dir):
     S, N, covered = lru.cache_geometry(ex["slots"] * per_expert, per_expert, ex["ways"], 32)
     assert (S, N) == (ex["slots"], ex["indexes"])
     assert (covered[0], covered[-1]) == tuple(ex["covered_layers"])
-    # from memory sizes: (24 - 5) GB / 340 MB is "around 56" slots
+    # from memory sizes: (24 - 5) GB / 340 MB gives about 56 slots
     S2, _, _ = lru.cache_geometry((ex["gpu_GB"] - ex["non_expert_GB"]) * 10**9, ex["per_expert_MB"] * 10**6, 4, 32)
     assert abs(S2 - ex["slots"]) <= 2
     assert 8 * 32 == ex["total_experts"]
